@@ -1,0 +1,503 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test checks the oracle by a route other than its own code: closed forms,
+brute force on tiny inputs, special cases that reduce to a textbook or
+library routine, invariants the paper states, a hand-worked example with
+dyadic numbers, and the storage figure the projector ablation table prints.
+"""
+
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+from scipy.special import expit
+
+from oracle import exfold_oracle as O
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def rand_layer(rng, n=8, d=16, inter=8, shared=0, scale=0.3):
+    gu = (rng.standard_normal((n, 2 * inter, d)) * scale).astype(np.float32)
+    dn = (rng.standard_normal((n, d, inter)) * scale).astype(np.float32)
+    wr = (rng.standard_normal((n, d)) * scale).astype(np.float32)
+    sh = {}
+    if shared:
+        sh = dict(ws_gate_up=(rng.standard_normal((2 * shared, d)) * scale).astype(np.float32),
+                  ws_down=(rng.standard_normal((d, shared)) * scale).astype(np.float32))
+    return O.Layer(w_router=wr, w_gate_up=gu, w_down=dn, **sh)
+
+
+# ---------------------------------------------------------------- experts (Eq. gated_expert)
+
+def test_expert_scalar_closed_form():
+    rng = np.random.default_rng(1)
+    for _ in range(20):
+        wg, wu, wd, x = rng.standard_normal(4) * 2
+        gu = np.array([[wg], [wu]], dtype=np.float64)
+        dn = np.array([[wd]])
+        got = O.expert_forward(np.array([[x]]), gu, dn)[0, 0]
+        z = wg * x
+        want = wd * (z / (1.0 + math.exp(-z))) * (wu * x)
+        assert got == pytest.approx(want, rel=1e-14, abs=1e-300)
+
+
+def test_expert_diagonal_reduces_to_silu_times_x():
+    # W_gate = diag(a), W_up = I, W_down = I  =>  E(x) = SiLU(a*x) * x, SiLU = z * sigmoid(z)
+    rng = np.random.default_rng(2)
+    d = 6
+    a = rng.standard_normal(d)
+    gu = np.concatenate([np.diag(a), np.eye(d)])
+    x = rng.standard_normal((5, d)) * 3
+    got = O.expert_forward(x, gu, np.eye(d))
+    want = (a * x) * expit(a * x) * x
+    np.testing.assert_allclose(got, want, rtol=1e-13, atol=1e-15)
+    # gate and up are not interchangeable: swapping them changes the output
+    swapped = O.expert_forward(x, np.concatenate([np.eye(d), np.diag(a)]), np.eye(d))
+    assert not np.allclose(swapped, want)
+
+
+def test_expert_zero_and_down_linearity():
+    rng = np.random.default_rng(3)
+    gu = rng.standard_normal((8, 5))
+    dn = rng.standard_normal((5, 4))
+    assert np.all(O.expert_forward(np.zeros((2, 5)), gu, dn) == 0)
+    x = rng.standard_normal((3, 5))
+    np.testing.assert_array_equal(O.expert_forward(x, gu, 4.0 * dn), 4.0 * O.expert_forward(x, gu, dn))
+
+
+# ---------------------------------------------------------------- router (Eq. topk_gate)
+
+def test_router_logits_unit_vectors():
+    rng = np.random.default_rng(4)
+    wr = rng.standard_normal((5, 7))
+    b = rng.standard_normal(5)
+    got = O.router_logits(np.eye(7), wr, b)
+    np.testing.assert_array_equal(got, wr.T + b[None, :])
+
+
+def _check_topk_property(logits, ids):
+    n = logits.shape[1]
+    for i in range(logits.shape[0]):
+        row = logits[i].astype(np.float64)
+        sel = [int(e) for e in ids[i]]
+        assert len(set(sel)) == len(sel)
+        for a, b in zip(sel, sel[1:]):
+            assert row[a] > row[b] or (row[a] == row[b] and a < b)
+        last = sel[-1]
+        for e in range(n):
+            if e not in sel:
+                assert row[e] < row[last] or (row[e] == row[last] and e > last)
+
+
+def test_topk_order_property_with_ties():
+    rng = np.random.default_rng(5)
+    logits = rng.standard_normal((200, 16)).astype(np.float32)
+    logits[:, 3] = logits[:, 9]                  # exact ties between ids 3 and 9
+    logits[::7, :] = np.round(logits[::7, :])    # many ties on some rows
+    logits[5] = 0.0                              # all tied: ids 0..K-1
+    logits[6, 4] = -0.0                          # -0 ties +0
+    for k in (1, 2, 5, 16):
+        ids = O.topk_ids(logits, k)
+        _check_topk_property(logits, ids)
+        assert list(ids[5]) == list(range(k))
+
+
+def test_softmax_closed_forms():
+    rng = np.random.default_rng(6)
+    logits = rng.standard_normal((100, 10)).astype(np.float32) * 3
+    ids, w = O.route(logits, 4)
+    w64 = w.astype(np.float64)
+    np.testing.assert_allclose(w64.sum(axis=1), 1.0, atol=4 * 2.0 ** -24)
+    for i in range(0, 100, 9):
+        for a in range(4):
+            for b in range(4):
+                ratio = math.exp(float(logits[i, ids[i, a]]) - float(logits[i, ids[i, b]]))
+                assert w64[i, a] / w64[i, b] == pytest.approx(ratio, rel=4 * 2.0 ** -24)
+    # equal logits give uniform weights; K=1 gives exactly 1
+    _, wu = O.route(np.zeros((2, 8), np.float32), 4)
+    assert np.all(wu == np.float32(0.25))
+    _, w1 = O.route(logits, 1)
+    assert np.all(w1 == 1.0)
+
+
+# ---------------------------------------------------------------- prefill selection (Eq. prefill_budget)
+
+def test_prefill_select_bruteforce_subsets():
+    rng = np.random.default_rng(7)
+    for k, kp in [(4, 1), (4, 2), (6, 3), (8, 4), (8, 7)]:
+        ids = np.stack([rng.permutation(16)[:k] for _ in range(50)]).astype(np.int32)
+        w = rng.random((50, k)).astype(np.float32)
+        h = (rng.random(16) + 0.1).astype(np.float32)
+        keep = O.select_prefill(ids, w, h, kp)
+        for i in range(50):
+            score = [float(w[i, j]) * float(h[ids[i, j]]) for j in range(k)]
+            best = max(itertools.combinations(range(k), kp), key=lambda c: sum(score[j] for j in c))
+            assert set(np.nonzero(keep[i])[0]) == set(best)
+
+
+def test_prefill_select_constant_h_is_direct_topk():
+    rng = np.random.default_rng(8)
+    logits = rng.standard_normal((40, 12)).astype(np.float32)
+    ids, w = O.route(logits, 6)
+    keep = O.select_prefill(ids, w, np.full(12, 0.7, np.float32), 3)
+    assert np.all(keep[:, :3]) and not np.any(keep[:, 3:])
+    # all scores tied -> first K' route positions
+    keep = O.select_prefill(ids, np.full_like(w, 0.25), np.ones(12, np.float32), 2)
+    assert np.all(keep[:, :2]) and not np.any(keep[:, 2:])
+
+
+# ---------------------------------------------------------------- prefill fold (Eq. prefill_fold)
+
+def test_prefill_fold_hand_worked_example():
+    # routes (5, 2, 7, 0), w = (1/2, 1/4, 1/8, 1/8); h5=1, h2=4, h7=2, h0=1
+    # scores (1/2, 1, 1/4, 1/8) -> K'=2 keeps ids 5 and 2, listed in route order.
+    # omitted 7: L[7,5]=1/2 > L[7,2]=1/4 -> target 2, S[7,2]=2: w~2 = 1/4 + 1/8*2 = 1/2
+    # omitted 0: L[0,5] = L[0,2] -> first in route order -> 5, S[0,5]=-1: w~5 = 1/2 - 1/8 = 3/8
+    n = 8
+    ids = np.array([[5, 2, 7, 0]], np.int32)
+    w = np.array([[0.5, 0.25, 0.125, 0.125]], np.float32)
+    h = np.ones(n, np.float32)
+    h[2], h[7] = 4.0, 2.0
+    S = np.zeros((n, n), np.float32)
+    L = np.ones((n, n), np.float32)
+    L[7, 5], L[7, 2], S[7, 2] = 0.5, 0.25, 2.0
+    L[0, 5], L[0, 2], S[0, 5] = 0.1, 0.1, -1.0
+    keep = O.select_prefill(ids, w, h, 2)
+    assert keep.tolist() == [[True, True, False, False]]
+    out_ids, out_w = O.fold_prefill(ids, w, keep, S, L)
+    assert out_ids.tolist() == [[5, 2]]
+    assert out_w.tolist() == [[0.375, 0.5]]
+
+
+def test_prefill_fold_properties():
+    rng = np.random.default_rng(9)
+    n, k, kp, t = 16, 8, 3, 60
+    ids = np.stack([rng.permutation(n)[:k] for _ in range(t)]).astype(np.int32)
+    w = rng.random((t, k)).astype(np.float32)
+    h = rng.random(n).astype(np.float32)
+    S = rng.standard_normal((n, n)).astype(np.float32)
+    L = rng.random((n, n)).astype(np.float32)
+    L[:, 3] = L[:, 5]                                   # ties in the loss table
+    keep = O.select_prefill(ids, w, h, kp)
+    out_ids, out_w = O.fold_prefill(ids, w, keep, S, L)
+    assert out_ids.shape == (t, kp)
+    for i in range(t):
+        ret = [j for j in range(k) if keep[i, j]]
+        assert out_ids[i].tolist() == [int(ids[i, j]) for j in ret]       # route order
+        expect = {j: float(w[i, j]) for j in ret}
+        for j in range(k):
+            if keep[i, j]:
+                continue
+            s = int(ids[i, j])
+            cand = [int(ids[i, r]) for r in ret]
+            tpos = int(np.argmin(L[s, cand]))                           # numpy: first minimum
+            expect[ret[tpos]] += float(w[i, j]) * float(S[s, cand[tpos]])
+        np.testing.assert_array_equal(out_w[i], np.array([expect[j] for j in ret], np.float32))
+    # S == 0: direct Top-K' drop, weights not renormalised
+    _, w0 = O.fold_prefill(ids, w, keep, np.zeros_like(S), L)
+    np.testing.assert_array_equal(w0, np.stack([w[i][keep[i]] for i in range(t)]))
+    # S == 1: routed mass conserved
+    _, w1 = O.fold_prefill(ids, w, keep, np.ones_like(S), L)
+    np.testing.assert_allclose(w1.astype(np.float64).sum(1), w.astype(np.float64).sum(1), rtol=1e-6)
+
+
+def test_prefill_identity_budget_is_bitwise():
+    rng = np.random.default_rng(10)
+    logits = rng.standard_normal((30, 12)).astype(np.float32)
+    ids, w = O.route(logits, 4)
+    for kp in (4, 5, 100):
+        keep = O.select_prefill(ids, w, rng.random(12).astype(np.float32), kp)
+        oi, ow = O.fold_prefill(ids, w, keep, rng.random((12, 12)), rng.random((12, 12)))
+        assert np.array_equal(oi, ids) and np.array_equal(ow.view(np.uint32), w.view(np.uint32))
+
+
+# ---------------------------------------------------------------- decode pool (Eq. decode_budget)
+
+def test_decode_hand_worked_example():
+    # token0 (1, 3) w (3/4, 1/4); token1 (3, 0) w (1/2, 1/2); token2 (2, 1) w (1/2, 1/2); h = (1, 1, 2, 1)
+    # sum_w: e0 1/2, e1 5/4, e2 1/2, e3 3/4 -> scores 1/2, 5/4, 1, 3/4 -> D=2 pool (1, 2)
+    # source 0: L[0,1]=.3 > L[0,2]=.2 -> 2, S=1/2;  source 3: L[3,1] = L[3,2] -> pool order -> 1, S=3
+    ids = np.array([[1, 3], [3, 0], [2, 1]], np.int32)
+    w = np.array([[0.75, 0.25], [0.5, 0.5], [0.5, 0.5]], np.float32)
+    h = np.array([1, 1, 2, 1], np.float32)
+    pool, cand = O.select_decode_pool(ids, w, h, 4, 2)
+    assert pool == [1, 2] and cand == [0, 1, 2, 3]
+    S = np.zeros((4, 4), np.float32)
+    L = np.ones((4, 4), np.float32)
+    L[0, 1], L[0, 2], S[0, 2] = 0.3, 0.2, 0.5
+    L[3, 1], L[3, 2], S[3, 1] = 0.4, 0.4, 3.0
+    ni, nw, tgt, scl = O.fold_decode(ids, w, pool, S, L, 4)
+    assert ni.tolist() == [[1, 1], [1, 2], [2, 1]]
+    assert nw.tolist() == [[0.75, 0.75], [1.5, 0.25], [0.5, 0.5]]
+    assert tgt.tolist() == [2, 1, 2, 1] and scl.tolist() == [0.5, 1.0, 1.0, 3.0]
+
+
+def test_decode_pool_bruteforce_and_fixed_point_bound():
+    rng = np.random.default_rng(11)
+    n, k = 10, 3
+    for trial in range(30):
+        b = int(rng.integers(1, 6))
+        ids = np.stack([rng.permutation(n)[:k] for _ in range(b)]).astype(np.int32)
+        w = rng.random((b, k)).astype(np.float32)
+        h = (rng.random(n) + 0.05).astype(np.float32)
+        dd = int(rng.integers(1, 7))
+        pool, cand = O.select_decode_pool(ids, w, h, n, dd)
+        assert cand == sorted(set(ids.reshape(-1).tolist()))
+        assert len(pool) == min(dd, len(cand)) and set(pool) <= set(cand)
+        real = {e: sum(float(w[i, j]) for i in range(b) for j in range(k) if ids[i, j] == e) * float(h[e])
+                for e in cand}
+        best = max(itertools.combinations(cand, len(pool)), key=lambda c: sum(real[e] for e in c))
+        assert set(pool) == set(best)
+        # pool order is descending real-valued score
+        assert all(real[a] >= real[c] for a, c in zip(pool, pool[1:]))
+        # R6 deviation bound: |fixed-point score - real score| <= slots * 2^-41 * h
+        scale = 2.0 ** 40
+        for e in cand:
+            fx = sum(int(np.rint(float(w[i, j]) * scale)) for i in range(b) for j in range(k) if ids[i, j] == e)
+            assert abs(fx / scale * float(h[e]) - real[e]) <= b * 2.0 ** -41 * float(h[e]) + 1e-15
+
+
+def test_decode_pool_ties_lower_id():
+    ids = np.array([[0, 1], [2, 3]], np.int32)
+    w = np.full((2, 2), 0.5, np.float32)
+    pool, _ = O.select_decode_pool(ids, w, np.ones(4, np.float32), 4, 3)
+    assert pool == [0, 1, 2]
+
+
+def test_decode_fold_invariants_and_identity():
+    rng = np.random.default_rng(12)
+    n, k = 32, 4
+    S = rng.standard_normal((n, n)).astype(np.float32)
+    L = rng.random((n, n)).astype(np.float32)
+    for b in (1, 3, 17, 64):
+        logits = rng.standard_normal((b, n)).astype(np.float32)
+        ids, w = O.route(logits, k)
+        h = rng.random(n).astype(np.float32)
+        for dd in (1, 2, 5, 16, n):
+            pool, cand = O.select_decode_pool(ids, w, h, n, dd)
+            ni, nw, tgt, scl = O.fold_decode(ids, w, pool, S, L, n)
+            assert ni.shape == ids.shape and nw.shape == w.shape
+            assert len(set(ni.reshape(-1).tolist())) <= dd
+            assert set(ni.reshape(-1).tolist()) <= set(pool)
+            kept = np.isin(ids, pool)
+            assert np.array_equal(ni[kept], ids[kept])
+            assert np.array_equal(nw[kept].view(np.uint32), w[kept].view(np.uint32))
+            # remapped weight == float32 multiply (numpy float32 arithmetic)
+            moved = ~kept
+            np.testing.assert_array_equal(nw[moved], (w * S[ids, ni])[moved])
+            for s in range(n):
+                if s not in pool:
+                    assert tgt[s] == pool[int(np.argmin(L[s, pool]))]
+            if dd >= len(cand):
+                assert np.array_equal(ni, ids) and np.array_equal(nw.view(np.uint32), w.view(np.uint32))
+
+
+def test_static_pool():
+    h = np.array([0.5, 2.0, 2.0, 1.0, 0.1], np.float32)
+    assert O.select_static_pool(h, 3) == [1, 2, 3]
+    assert sorted(O.select_static_pool(h, 5)) == list(range(5))
+    # D = N: every source is in the pool, the remap is the identity
+    ids = np.array([[4, 0], [2, 1]], np.int32)
+    w = np.array([[0.6, 0.4], [0.7, 0.3]], np.float32)
+    ni, nw, _, _ = O.fold_decode(ids, w, O.select_static_pool(h, 5), np.zeros((5, 5)), np.ones((5, 5)), 5)
+    assert np.array_equal(ni, ids) and np.array_equal(nw, w)
+
+
+# ---------------------------------------------------------------- permutation
+
+def test_permutation_matches_stable_argsort():
+    rng = np.random.default_rng(13)
+    for shape, n in [((64, 1), 8), ((100, 8), 128), ((1, 3), 4), ((0, 4), 5), ((37, 2), 3)]:
+        ids = rng.integers(0, n, size=shape).astype(np.int32)
+        counts, offsets, row_slot = O.permute_routes(ids, n)
+        flat = ids.reshape(-1)
+        np.testing.assert_array_equal(counts, np.bincount(flat, minlength=n))
+        np.testing.assert_array_equal(offsets, np.concatenate([[0], np.cumsum(np.bincount(flat, minlength=n))]))
+        np.testing.assert_array_equal(row_slot, np.argsort(flat, kind="stable"))
+
+
+# ---------------------------------------------------------------- layer output (Eq. moe_output)
+
+def test_moe_output_equals_dense_masked_sum():
+    """All N experts evaluated on every token, combined through a dense [T, N] gate matrix."""
+    rng = np.random.default_rng(14)
+    layer = rand_layer(rng, n=8, d=12, inter=6, shared=5)
+    x = rng.standard_normal((9, 12)).astype(np.float32)
+    ids = rng.integers(0, 8, size=(9, 3)).astype(np.int32)     # duplicates allowed (decode remap)
+    w = rng.standard_normal((9, 3)).astype(np.float32)
+    alpha = np.zeros((9, 8))
+    for i in range(9):
+        for j in range(3):
+            alpha[i, ids[i, j]] += float(w[i, j])
+    dense = sum(alpha[:, e:e + 1] * O.expert_forward(x, *layer.expert(e)) for e in range(8))
+    dense = dense + O.expert_forward(x, layer.ws_gate_up, layer.ws_down)
+    np.testing.assert_allclose(O.moe_output(layer, x, ids, w), dense, rtol=1e-12, atol=1e-13)
+
+
+def test_identity_budgets_give_bitwise_dense_output():
+    rng = np.random.default_rng(15)
+    layer = rand_layer(rng, n=8, d=12, inter=6)
+    x = rng.standard_normal((20, 12)).astype(np.float32)
+    S = rng.standard_normal((8, 8)).astype(np.float32)
+    L = rng.random((8, 8)).astype(np.float32)
+    h = rng.random(8).astype(np.float32)
+    y0, _ = O.moe_forward(layer, x, 3, "dense", 0)
+    yp, _ = O.moe_forward(layer, x, 3, "prefill", 3, S, L, h)
+    yd, info = O.moe_forward(layer, x, 3, "decode", 8, S, L, h)
+    assert np.array_equal(y0, yp) and np.array_equal(y0, yd)
+
+
+def test_fold_then_execute_equals_definition():
+    """Eq. folded_moe term by term vs coalesced prefill fold and in-place decode remap."""
+    rng = np.random.default_rng(16)
+    n = 8
+    layer = rand_layer(rng, n=n, d=10, inter=6, shared=4)
+    x = rng.standard_normal((15, 10)).astype(np.float32)
+    S = rng.standard_normal((n, n)).astype(np.float32)
+    L = rng.random((n, n)).astype(np.float32)
+    h = rng.random(n).astype(np.float32)
+    logits = O.router_logits(x, layer.w_router)
+    ids, w = O.route(logits, 4)
+    # prefill, K' = 2
+    y_fold, info = O.moe_forward(layer, x, 4, "prefill", 2, S, L, h)
+    sets = [[int(ids[i, j]) for j in range(4) if info["keep"][i, j]] for i in range(15)]
+    y_def = O.folded_output_by_definition(layer, x, ids, w, sets, S, L)
+    np.testing.assert_allclose(y_fold, y_def, rtol=1e-6, atol=1e-7)  # w~ is stored as float32
+    # decode, D = 3
+    y_fold, info = O.moe_forward(layer, x, 4, "decode", 3, S, L, h)
+    y_def = O.folded_output_by_definition(layer, x, ids, w, [info["pool"]] * 15, S, L)
+    np.testing.assert_allclose(y_fold, y_def, rtol=1e-6, atol=1e-7)
+
+
+# ---------------------------------------------------------------- calibration (Eq. scalar_projector, projection_loss)
+
+def twin_layer(rng, d=16, inter=8, c=(0.5, -1.0, 2.0, -0.5)):
+    """Experts 4+j copy gate/up of expert j and scale its down projection by c_j (a power of two)."""
+    base = rand_layer(rng, n=4, d=d, inter=inter)
+    gu = np.concatenate([base.w_gate_up, base.w_gate_up])
+    dn = np.concatenate([base.w_down, np.stack([np.float32(cj) * base.w_down[j] for j, cj in enumerate(c)])])
+    wr = (rng.standard_normal((8, d)) * 0.3).astype(np.float32)
+    return O.Layer(w_router=wr, w_gate_up=gu, w_down=dn)
+
+
+def test_exact_multiples_calibrate_to_exact_scalars_and_fold_exactly():
+    rng = np.random.default_rng(17)
+    c = (0.5, -1.0, 2.0, -0.5)
+    layer = twin_layer(rng, c=c)
+    xc = rng.standard_normal((40, 16)).astype(np.float32)
+    S, L, h, st = O.calibrate(layer, xc, 2, lam=0.0, clip=4.0, mode="common")
+    for j, cj in enumerate(c):
+        assert st["S64"][4 + j, j] == cj and st["S64"][j, 4 + j] == 1.0 / cj
+        assert st["L64"][4 + j, j] == 0.0 and st["L64"][j, 4 + j] == 0.0
+    off = [(s, t) for s in range(8) for t in range(8) if s != t and abs(s - t) != 4]
+    assert min(st["L64"][s, t] for s, t in off) > 0.0
+    x = rng.standard_normal((24, 16)).astype(np.float32)
+    # prefill: every token routes one twin pair; K' = 1
+    j = rng.integers(0, 4, 24)
+    flip = rng.random(24) < 0.5
+    ids = np.stack([np.where(flip, j + 4, j), np.where(flip, j, j + 4)], 1).astype(np.int32)
+    w = rng.random((24, 2)).astype(np.float32)
+    keep = O.select_prefill(ids, w, h, 1)
+    fi, fw = O.fold_prefill(ids, w, keep, S, L)
+    y = O.moe_output(layer, x, ids, w)
+    np.testing.assert_allclose(O.moe_output(layer, x, fi, fw), y, rtol=1e-6, atol=1e-9)  # fp32 metadata
+    # same in float64 metadata: exact up to float64 rounding
+    fw64 = np.array([float(w[i, keep[i]][0]) + float(w[i, ~keep[i]][0]) *
+                     float(S[ids[i, ~keep[i]][0], fi[i, 0]]) for i in range(24)])[:, None]
+    np.testing.assert_allclose(O.moe_output(layer, x, fi, fw64), y, rtol=1e-12, atol=1e-14)
+    # decode: pool of the four base experts (large h), every twin folds onto its base
+    hd = np.array([10, 10, 10, 10, 1, 1, 1, 1], np.float32)
+    ids4 = np.concatenate([ids, ids[::-1]], 1)
+    w4 = rng.random((24, 4)).astype(np.float32)
+    pool, _ = O.select_decode_pool(ids4, w4, hd, 8, 4)
+    assert sorted(pool) == [0, 1, 2, 3]
+    ni, nw, tgt, scl = O.fold_decode(ids4, w4, pool, S, L, 8)
+    assert tgt.tolist()[4:] == [0, 1, 2, 3] and scl.tolist()[4:] == list(c)
+    np.testing.assert_allclose(O.moe_output(layer, x, ni, nw), O.moe_output(layer, x, ids4, w4),
+                               rtol=1e-12, atol=1e-14)
+
+
+def _pair_samples(layer, xc, top_k, mode):
+    logits = O.router_logits(xc, layer.w_router)
+    ids = O.topk_ids(logits, top_k)
+    outs = np.stack([O.expert_forward(xc, *layer.expert(e)) for e in range(layer.n_experts)])
+    ev = [list(map(int, ids[i])) if mode == "corouted" else list(range(layer.n_experts))
+          for i in range(xc.shape[0])]
+    return outs, ev
+
+
+@pytest.mark.parametrize("mode", ["corouted", "common"])
+def test_scalar_projector_is_weighted_ridge_least_squares(mode):
+    rng = np.random.default_rng(18)
+    layer = rand_layer(rng, n=5, d=8, inter=6)
+    xc = rng.standard_normal((30, 8)).astype(np.float32)
+    lam = 0.37
+    S, L, h, st = O.calibrate(layer, xc, 2, lam=lam, clip=0.0, mode=mode)
+    outs, ev = _pair_samples(layer, xc, 2, mode)
+    checked = 0
+    for s in range(5):
+        for t in range(5):
+            toks = [i for i in range(30) if s in ev[i] and t in ev[i]]
+            if s == t or not toks:
+                continue
+            rows = [math.sqrt(np.linalg.norm(outs[s, i])) * outs[t, i] for i in toks]
+            rhs = [math.sqrt(np.linalg.norm(outs[s, i])) * outs[s, i] for i in toks]
+            M = np.concatenate(rows + [np.array([math.sqrt(lam)])])[:, None]
+            r = np.concatenate(rhs + [np.array([0.0])])
+            sol = np.linalg.lstsq(M, r, rcond=None)[0][0]
+            assert st["S64"][s, t] == pytest.approx(sol, rel=1e-10, abs=1e-14)
+            # Eq. projection_loss evaluated directly from the samples
+            wts = [np.linalg.norm(outs[s, i]) for i in toks]
+            num = sum(wi * np.sum((outs[s, i] - sol * outs[t, i]) ** 2) for wi, i in zip(wts, toks))
+            den = sum(wi * np.sum(outs[s, i] ** 2) for wi, i in zip(wts, toks)) + O.EPSILON
+            assert st["L64"][s, t] == pytest.approx(num / den, rel=1e-9, abs=1e-12)
+            checked += 1
+    assert checked > 0
+
+
+def test_calibration_edge_cases():
+    rng = np.random.default_rng(19)
+    layer = rand_layer(rng, n=8, d=8, inter=4)
+    xc = rng.standard_normal((3, 8)).astype(np.float32)          # few tokens: most pairs unobserved
+    S, L, h, st = O.calibrate(layer, xc, 2)
+    assert np.all(np.diag(S) == 1.0) and np.all(np.diag(L) == 0.0)
+    unobs = (st["n"] == 0) & ~np.eye(8, dtype=bool)
+    assert unobs.any()
+    assert np.all(S[unobs] == 0.0) and np.all(L[unobs] == np.float32(1e30))
+    assert np.all(np.abs(S) <= 4.0)
+    # h: mean output norm over tokens routed to the expert; unrouted experts get the mean of observed
+    outs, ev = _pair_samples(layer, xc, 2, "corouted")
+    seen = sorted(set(e for row in ev for e in row))
+    for e in seen:
+        want = np.mean([np.linalg.norm(outs[e, i]) for i in range(3) if e in ev[i]])
+        assert float(h[e]) == pytest.approx(want, rel=1e-6)
+    for e in set(range(8)) - set(seen):
+        assert float(h[e]) == pytest.approx(np.mean([float(st["h64"][s]) for s in seen]), rel=1e-6)
+
+
+def test_clipped_scalar_defines_the_loss():
+    # E_s = 8 E_t: unclipped s = 8; clipped to 4, the loss is ||8v - 4v||^2 / ||8v||^2 = 1/4
+    rng = np.random.default_rng(20)
+    layer = twin_layer(rng, c=(8.0, 1.0, 1.0, 1.0))
+    xc = rng.standard_normal((10, 16)).astype(np.float32)
+    S, L, h, st = O.calibrate(layer, xc, 2, lam=0.0, clip=4.0, mode="common")
+    assert st["S64"][4, 0] == 4.0
+    assert st["L64"][4, 0] == pytest.approx(0.25, rel=1e-12)
+    _, _, _, st0 = O.calibrate(layer, xc, 2, lam=0.0, clip=0.0, mode="common")
+    assert st0["S64"][4, 0] == 8.0 and st0["L64"][4, 0] == 0.0
+
+
+def test_storage_matches_projector_ablation_table():
+    rows = {}
+    with open(os.path.join(HERE, "golden", "projector_storage.txt")) as f:
+        for line in f:
+            if line.strip() and not line.startswith("#"):
+                fam, val, unit = line.split()
+                rows[fam] = (float(val), unit)
+    units = {"B": 1, "MiB": 2 ** 20}
+    for fam, (val, unit) in rows.items():
+        got = O.table_storage_bytes(48, 128, fam) / units[unit]
+        assert f"{got:.2f}" == f"{val:.2f}", fam
