@@ -1,0 +1,283 @@
+#!/usr/bin/env python3
+"""Benchmark of the folded MoE layer on one MI355X.
+
+Default workload: the Mixtral-8x7B-shaped layer (bf16, hidden 4096, 8 experts,
+top-2, intermediate 14336).  One step = one prefill forward (4096 tokens,
+K'=1 token-level folding) + one decode forward (32 tokens, pool of 4 of 8
+experts), each the whole folded layer: router, Top-K, selection, fold,
+permutation, grouped SwiGLU GEMMs, combine.  Inputs are seeded synthetic data
+resident in HBM before the timed region; the projector tables are seeded
+stand-ins (their values only steer selection, not the amount of work).
+
+Prints ONE JSON line: value = prefill TFLOP/s (algorithmic flops / mean
+prefill-layer time), with the decode layer's us/layer and HBM GB/s, the
+roofline of the dominant kernel (the prefill gate/up GEMM, timed live with
+HIP events on its stream) and the CPU oracle timed on a bounded sample.
+
+    python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload mixtral|qwen3|glm|qwen3-decode]
+"""
+
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "folded MoE layer: prefill TFLOP/s + %MFMA peak; decode µs/layer + HBM GB/s"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+class HipEvents:
+    """hipEvent_t handles from the HIP runtime torch has loaded (one runtime per process)."""
+
+    def __init__(self):
+        import torch
+        path = os.path.join(os.path.dirname(torch.__file__), "lib", "libamdhip64.so")
+        self.hip = ctypes.CDLL(path if os.path.exists(path) else "libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p, ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        self.owned = []
+
+    def array(self, n):
+        arr = (ctypes.c_void_p * n)()
+        for i in range(n):
+            ev = ctypes.c_void_p()
+            assert self.hip.hipEventCreate(ctypes.byref(ev)) == 0
+            arr[i] = ev.value
+            self.owned.append(ev.value)
+        return arr
+
+    def record(self, ev, stream):
+        assert self.hip.hipEventRecord(ev, stream) == 0
+
+    def ms(self, a, b):
+        out = ctypes.c_float()
+        assert self.hip.hipEventElapsedTime(ctypes.byref(out), a, b) == 0
+        return float(out.value)
+
+    def close(self):
+        for ev in self.owned:
+            self.hip.hipEventDestroy(ev)
+        self.owned = []
+
+
+def make_layer(shape, seed=0):
+    import numpy as np
+    import torch
+    from paper_2608_24938_amd import exfold as X
+    from paper_2608_24938_amd import synth
+
+    def dev(a):
+        if a is None:
+            return None
+        if a.dtype == np.uint16:
+            return torch.from_numpy(a.view(np.int16)).to("cuda").view(torch.bfloat16)
+        return torch.from_numpy(a).to("cuda")
+
+    wr = synth.router_weight(shape, seed)
+    gu, dn = synth.all_expert_weights(shape, seed, threads=16)
+    sgu, sdn = synth.shared_weights(shape, seed)
+    layer = X.Layer(w_router=dev(wr), w_gate_up=dev(gu), w_down=dev(dn), top_k=shape.top_k,
+                    router_bias=dev(synth.router_bias(shape, seed)), ws_gate_up=dev(sgu), ws_down=dev(sdn))
+    host = dict(wr=wr, gu=gu, dn=dn, sgu=sgu, sdn=sdn, bias=synth.router_bias(shape, seed))
+    return layer, host, dev
+
+
+def prefill_flops(shape, T, k_out):
+    """Algorithmic flops of one prefill layer: router GEMM + gate/up (4dI) and down (2dI) per executed route."""
+    shared = 6 * shape.d * shape.shared_inter * T
+    return 2 * shape.d * shape.n_experts * T + 6 * shape.d * shape.inter * T * k_out + shared
+
+
+def decode_bytes(shape, B, touched):
+    """Algorithmic HBM bytes of one decode layer: weights of the touched experts (+ shared), router, x and y."""
+    esz = 2 if shape.dtype == "bf16" else 4
+    w = 3 * shape.d * shape.inter * esz * touched + 3 * shape.d * shape.shared_inter * esz
+    return w + shape.n_experts * shape.d * esz + 2 * B * shape.d * esz + B * shape.top_k * 16
+
+
+def run_phase(X, layer, x, phase, budget, tables, steps, warmup, ev, stream, dbg=None):
+    """Warm up, then time `steps` forwards; returns per-step stage durations (ms)."""
+    import torch
+    S, L, h = tables
+    y = torch.empty_like(x)
+    ws = torch.empty(X.moe_workspace_size(layer, x.shape[0], phase, budget), dtype=torch.uint8, device="cuda")
+    for _ in range(warmup):
+        X.moe_forward(layer, x, phase, budget, S, L, h, y=y, workspace=ws, debug=dbg)
+    torch.cuda.synchronize()
+    arrs = [ev.array(X.N_EVENTS) for _ in range(steps)]
+    return y, ws, arrs
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="mixtral", choices=["mixtral", "qwen3", "glm", "qwen3-decode"])
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the folded layer is measured "
+              f"on a single MI355X and no multi-GPU path is built.", file=sys.stderr)
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    from paper_2608_24938_amd import exfold as X
+    from paper_2608_24938_amd import synth
+
+    X.lib()  # fail loudly if the library is missing
+    torch.cuda.init()
+    props = torch.cuda.get_device_properties(0)
+    log(f"device: {props.name} CUs={props.multi_processor_count}")
+
+    if args.workload == "mixtral":
+        shape = synth.MIXTRAL
+        prefill = (4096, 1)
+        decode = (32, 4)
+        workload = "mixtral-8x7b-shaped MoE layer (d=4096, 8 experts, top-2, I=14336, bf16): " \
+                   "prefill 4096 tokens K'=1 + decode 32 tokens pool D=4"
+    elif args.workload == "qwen3":
+        shape = synth.QWEN3
+        prefill = (8192, 4)
+        decode = (64, 32)
+        workload = "qwen3-30b-a3b-shaped MoE layer (d=2048, 128 experts, top-8, I=768, skewed router, bf16): " \
+                   "prefill 8192 tokens K'=4 + decode 64 tokens pool D=32"
+    elif args.workload == "glm":
+        shape = synth.GLM45
+        prefill = (4096, 4)
+        decode = (64, 32)
+        workload = "glm-4.5-air-shaped MoE layer (d=4096, 128 experts + 1 shared, top-8, I=1408, bf16): " \
+                   "prefill 4096 tokens K'=4 + decode 64 tokens pool D=32"
+    else:
+        shape = synth.QWEN3_DECODE
+        prefill = (512, 4)
+        decode = (128, 16)
+        workload = "qwen3-30b-a3b-shaped MoE layer (bf16): prefill 512 tokens K'=4 + decode 128 tokens pool D=16"
+
+    t0 = time.time()
+    layer, host, dev = make_layer(shape, seed=0)
+    T, kp = prefill
+    B, D = decode
+    xs_p = synth.tokens(shape, T, seed=0)
+    xs_d = synth.tokens(shape, B, seed=1)
+    x_p, x_d = dev(xs_p), dev(xs_d)
+    S_np, L_np, h_np = synth.synthetic_tables(shape.n_experts, seed=0)
+    tables = (dev(S_np), dev(L_np), dev(h_np))
+    torch.cuda.synchronize()
+    log(f"inputs ready in {time.time() - t0:.1f}s")
+
+    stream = torch.cuda.current_stream()
+    sptr = ctypes.c_void_p(stream.cuda_stream)
+    ev = HipEvents()
+    dbg_d = {"pool_size": torch.empty(1, dtype=torch.int32, device="cuda")}
+    S, L, h = tables
+    y_p, ws_p, ev_p = run_phase(X, layer, x_p, "prefill", kp, tables, args.steps, args.warmup, ev, stream)
+    y_d, ws_d, ev_d = run_phase(X, layer, x_d, "decode", D, tables, args.steps, args.warmup, ev, stream, dbg_d)
+    edge = ev.array(2)
+    torch.cuda.synchronize()
+    # ---- timed region: exactly `steps` steps, synchronised on both sides ----
+    ev.record(edge[0], sptr)
+    for k in range(args.steps):
+        X.moe_forward(layer, x_p, "prefill", kp, S, L, h, y=y_p, workspace=ws_p, events=ev_p[k])
+        X.moe_forward(layer, x_d, "decode", D, S, L, h, y=y_d, workspace=ws_d, events=ev_d[k], debug=dbg_d)
+    ev.record(edge[1], sptr)
+    torch.cuda.synchronize()
+    total_ms = ev.ms(edge[0], edge[1])
+    names = X.EVENT_NAMES
+
+    def stages(arrs):
+        out = {}
+        for i in range(1, len(names)):
+            out[names[i]] = float(np.mean([ev.ms(a[i - 1], a[i]) for a in arrs])) * 1e3
+        out["layer"] = float(np.mean([ev.ms(a[0], a[len(names) - 1]) for a in arrs])) * 1e3
+        return out
+
+    st_p, st_d = stages(ev_p), stages(ev_d)
+    touched = int(dbg_d["pool_size"].item())
+    flops_p = prefill_flops(shape, T, kp)
+    tflops = flops_p / (st_p["layer"] * 1e-6) / 1e12
+    gu_flops = 4 * shape.d * shape.inter * (T * kp + (T if shape.shared_inter else 0))
+    gu_tflops = gu_flops / (st_p["gate_up"] * 1e-6) / 1e12
+    bytes_d = decode_bytes(shape, B, touched)
+    gbs_d = bytes_d / (st_d["layer"] * 1e-6) / 1e9
+    log(f"prefill stages (us): {json.dumps({k: round(v, 1) for k, v in st_p.items()})}")
+    log(f"decode stages (us): {json.dumps({k: round(v, 1) for k, v in st_d.items()})}")
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(shape, host, xs_p, (S_np, L_np, h_np), kp)
+
+    rec = {
+        "metric": METRIC,
+        "value": round(tflops, 2),
+        "unit": "TFLOP/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(total_ms / args.steps, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded N(0,1) tokens, N(0,0.02^2) weights, seeded stand-in projector tables)",
+        "config": {"workload": workload, "prefill_tokens": T, "k_pre": kp, "decode_tokens": B, "pool_budget": D},
+        "prefill": {"us_per_layer": round(st_p["layer"], 1), "tflops": round(tflops, 2),
+                    "frac_mfma_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
+                    "algorithmic_gflop": round(flops_p / 1e9, 2), "stages_us": {k: round(v, 1) for k, v in st_p.items()}},
+        "decode": {"us_per_layer": round(st_d["layer"], 1), "hbm_gbs": round(gbs_d, 1),
+                   "frac_hbm_peak": round(gbs_d / PEAK_HBM_GBS, 4), "experts_touched": touched,
+                   "algorithmic_mb": round(bytes_d / 1e6, 2), "stages_us": {k: round(v, 1) for k, v in st_d.items()}},
+        "roofline": {"bound": "mfma", "achieved": round(gu_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                     "kernel": "expert_gemm_bf16 gate/up (+SiLU*up), prefill",
+                     "per_launch_gflop": round(gu_flops / 1e9, 2), "avg_launch_us": round(st_p["gate_up"], 1)},
+        "cpu_baseline": cpu,
+    }
+    ev.close()
+    print(json.dumps(rec), flush=True)
+
+
+def cpu_baseline(shape, host, xs_p, tables, kp, n_tokens=32):
+    """The oracle, as it stands, on the first n_tokens of the prefill batch (folded layer)."""
+    import numpy as np
+    from oracle import exfold_oracle as O
+    from paper_2608_24938_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [os.cpu_count()])
+    except Exception:
+        threads = os.cpu_count()
+    widen = synth.widen
+    ref = O.Layer(w_router=widen(host["wr"]), w_gate_up=lambda e: widen(host["gu"][e]),
+                  w_down=lambda e: widen(host["dn"][e]), router_bias=host["bias"],
+                  ws_gate_up=None if host["sgu"] is None else widen(host["sgu"]),
+                  ws_down=None if host["sdn"] is None else widen(host["sdn"]))
+    x = widen(xs_p[:n_tokens])
+    S, L, h = tables
+    t0 = time.perf_counter()
+    O.moe_forward(ref, x, shape.top_k, "prefill", kp, S, L, h)
+    dt = time.perf_counter() - t0
+    flops = prefill_flops(shape, n_tokens, kp)
+    log(f"cpu oracle: {n_tokens} tokens in {dt:.2f}s")
+    return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"first {n_tokens} of the {xs_p.shape[0]} prefill tokens, folded layer (float64 NumPy), "
+                      f"{dt:.2f} s wall", "seconds": round(dt, 3)}
+
+
+if __name__ == "__main__":
+    main()

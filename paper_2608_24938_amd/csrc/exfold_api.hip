@@ -1,0 +1,492 @@
+// C-ABI entry points of libexfold: argument validation (before any launch),
+// workspace planning, and the launch sequence of each call on the caller's
+// stream.  No host synchronisation, no device allocation.
+#include <hip/hip_runtime.h>
+
+#include <mutex>
+
+#include "common.hpp"
+#include "exfold.h"
+#include "kernels.hpp"
+
+using namespace exfold;
+
+namespace {
+
+constexpr size_t kAlign = 256;
+constexpr int64_t kMaxTokens = int64_t(1) << 22;  // keeps T*N and T*K_out*d offsets in range
+constexpr int64_t kMaxSlots = int64_t(1) << 28;
+
+inline size_t align_up(size_t x) { return (x + kAlign - 1) & ~(kAlign - 1); }
+
+struct Carver {
+  size_t off = 0;
+  size_t take(size_t bytes) {
+    const size_t o = off;
+    off = align_up(off + bytes);
+    return o;
+  }
+};
+
+// Read-only cache of the CU count per device (the only state the library keeps).
+int cu_count() {
+  static std::mutex mu;
+  static int cache[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  std::lock_guard<std::mutex> lock(mu);
+  if (cache[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0)
+      n = 256;
+    cache[dev] = n;
+  }
+  return cache[dev];
+}
+
+exfold_status check_layer(const exfold_layer *L) {
+  if (!L) return EXFOLD_ERR_NULL;
+  if (L->dtype != EXFOLD_F32 && L->dtype != EXFOLD_BF16) return EXFOLD_ERR_DTYPE;
+  if (!L->w_router || !L->w_gate_up || !L->w_down) return EXFOLD_ERR_NULL;
+  if (L->d <= 0 || L->inter <= 0 || L->n_experts <= 0 || L->top_k <= 0 || L->shared_inter < 0)
+    return EXFOLD_ERR_SHAPE;
+  if (L->top_k > L->n_experts) return EXFOLD_ERR_SHAPE;
+  if (L->n_experts > kMaxExperts || L->top_k > kMaxTopK) return EXFOLD_ERR_UNSUPPORTED;
+  if (L->d % 128 != 0 || L->inter % 64 != 0) return EXFOLD_ERR_UNSUPPORTED;
+  if (L->d > (1 << 16) || L->inter > (1 << 17)) return EXFOLD_ERR_UNSUPPORTED;
+  if (L->shared_inter > 0) {
+    if (!L->ws_gate_up || !L->ws_down) return EXFOLD_ERR_NULL;
+    if (L->shared_inter != L->inter) return EXFOLD_ERR_UNSUPPORTED;
+  }
+  return EXFOLD_OK;
+}
+
+exfold_status check_routing(int64_t T, int64_t N, int64_t K) {
+  if (T < 0 || N <= 0 || K <= 0 || K > N) return EXFOLD_ERR_SHAPE;
+  if (N > kMaxExperts || K > kMaxTopK) return EXFOLD_ERR_UNSUPPORTED;
+  if (T > kMaxTokens || T * K > kMaxSlots) return EXFOLD_ERR_SHAPE;
+  return EXFOLD_OK;
+}
+
+// Buffers of the expert stage (permutation, H, Y) for T tokens of k_out routes.
+struct ExecPlan {
+  int T = 0, k_out = 0, N = 0, d = 0, inter = 0, dtype = 0;
+  int t_shared = 0, R = 0, rows = 0, groups = 0;
+  bool direct = false;
+  GemmPlan gu{}, dn{};
+  size_t o_blk = 0, o_offsets = 0, o_ts0 = 0, o_ts1 = 0, o_row_token = 0, o_row_slot = 0,
+         o_row_w = 0, o_slot_row = 0, o_H = 0, o_Y = 0;
+};
+
+void plan_exec(const exfold_layer *L, int phase, int T, int k_out, bool with_shared,
+               bool keep_rows, int active_groups, Carver &c, ExecPlan &p) {
+  p.T = T;
+  p.k_out = k_out;
+  p.N = (int)L->n_experts;
+  p.d = (int)L->d;
+  p.inter = (int)L->inter;
+  p.dtype = L->dtype;
+  p.t_shared = (with_shared && L->shared_inter > 0) ? T : 0;
+  p.R = T * k_out;
+  p.rows = p.R + p.t_shared;
+  p.groups = p.N + (p.t_shared > 0 ? 1 : 0);
+  p.direct = !keep_rows && k_out == 1 && p.t_shared == 0;
+  (void)phase;
+  plan_expert_gemms(p.dtype, p.rows, p.groups, active_groups, p.d, p.inter, cu_count(), &p.gu,
+                    &p.dn);
+  if (p.direct || keep_rows) p.dn.ksplit = 1, p.dn.grid = (p.rows / p.dn.bm + p.groups) * (p.d / p.dn.bn);
+  if (p.dtype != EXFOLD_BF16) p.dn.ksplit = 1;
+  const int nblk = (p.R + kPermSlotsPerBlock - 1) / kPermSlotsPerBlock;
+  const size_t esz = (p.dtype == EXFOLD_BF16) ? 2 : 4;
+  p.o_blk = c.take(sizeof(int32_t) * (size_t)(nblk > 0 ? nblk : 1) * p.N);
+  p.o_offsets = c.take(sizeof(int32_t) * (p.N + 2));
+  p.o_ts0 = c.take(sizeof(int32_t) * (p.N + 2));
+  p.o_ts1 = c.take(sizeof(int32_t) * (p.N + 2));
+  p.o_row_token = c.take(sizeof(int32_t) * (size_t)p.rows);
+  p.o_row_slot = c.take(sizeof(int32_t) * (size_t)p.rows);
+  p.o_row_w = c.take(sizeof(float) * (size_t)p.rows);
+  p.o_slot_row = c.take(sizeof(int32_t) * (size_t)(p.R > 0 ? p.R : 1));
+  p.o_H = c.take(esz * (size_t)p.rows * p.inter);
+  p.o_Y = p.direct ? c.take(0) : c.take(sizeof(float) * (size_t)p.dn.ksplit * p.rows * p.d);
+}
+
+template <typename T> T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
+
+// Permutation, expert GEMMs and (unless keep_rows) the combine.
+inline void record(void *const *events, int i, hipStream_t s) {
+  if (events && events[i]) (void)hipEventRecord(static_cast<hipEvent_t>(events[i]), s);
+}
+
+exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
+                       const int32_t *route_ids, const float *route_w, void *y, void *ws,
+                       int32_t *offsets_dbg, int32_t *row_slot_dbg, bool keep_rows,
+                       hipStream_t s, void *const *events = nullptr) {
+  PermBuffers pb;
+  pb.blk_counts = at<int32_t>(ws, p.o_blk);
+  pb.offsets = offsets_dbg ? offsets_dbg : at<int32_t>(ws, p.o_offsets);
+  pb.tile_start0 = at<int32_t>(ws, p.o_ts0);
+  pb.tile_start1 = at<int32_t>(ws, p.o_ts1);
+  pb.row_token = at<int32_t>(ws, p.o_row_token);
+  pb.row_slot = row_slot_dbg ? row_slot_dbg : at<int32_t>(ws, p.o_row_slot);
+  pb.row_w = at<float>(ws, p.o_row_w);
+  pb.slot_row = at<int32_t>(ws, p.o_slot_row);
+  if (launch_permute(route_ids, route_w, p.T, p.k_out, p.N, p.t_shared, p.gu.bm, p.dn.bm, pb, s) !=
+      hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  record(events, EXFOLD_EV_PERMUTE, s);
+  ExpertArgs a{};
+  a.dtype = p.dtype;
+  a.d = p.d;
+  a.inter = p.inter;
+  a.n_experts = p.N;
+  a.groups = p.groups;
+  a.x = x;
+  a.w_gate_up = L->w_gate_up;
+  a.w_down = L->w_down;
+  a.ws_gate_up = L->ws_gate_up;
+  a.ws_down = L->ws_down;
+  a.offsets = pb.offsets;
+  a.tile_start_gu = pb.tile_start0;
+  a.tile_start_dn = pb.tile_start1;
+  a.row_token = pb.row_token;
+  a.row_w = pb.row_w;
+  a.rows = p.rows;
+  a.H = at<char>(ws, p.o_H);
+  a.Y = p.direct ? nullptr : at<float>(ws, p.o_Y);
+  a.y = y;
+  a.direct = p.direct;
+  hipEvent_t ev_mid = (events && events[EXFOLD_EV_GATE_UP])
+                          ? static_cast<hipEvent_t>(events[EXFOLD_EV_GATE_UP]) : nullptr;
+  if (launch_expert_gemms(a, p.gu, p.dn, s, ev_mid) != hipSuccess) return EXFOLD_ERR_DEVICE;
+  record(events, EXFOLD_EV_DOWN, s);
+  if (!p.direct && !keep_rows) {
+    if (launch_combine(p.dtype, a.Y, p.dn.ksplit, p.rows, pb.slot_row, p.T, p.k_out, p.d,
+                       p.t_shared > 0 ? p.R : -1, y, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+  }
+  record(events, EXFOLD_EV_END, s);
+  return EXFOLD_OK;
+}
+
+struct ForwardPlan {
+  int T = 0, N = 0, K = 0, k_out = 0, phase = 0, budget = 0, dcap = 0;
+  size_t o_logits = 0, o_topk_ids = 0, o_topk_w = 0, o_keep = 0, o_pool = 0, o_pool_size = 0,
+         o_tgt = 0, o_scl = 0, o_fold_ids = 0, o_fold_w = 0;
+  ExecPlan ex;
+  size_t total = 0;
+};
+
+exfold_status plan_forward(const exfold_layer *L, int64_t T, int32_t phase, int64_t budget,
+                           ForwardPlan &p) {
+  exfold_status st = check_layer(L);
+  if (st != EXFOLD_OK) return st;
+  if (phase != EXFOLD_PHASE_DENSE && phase != EXFOLD_PHASE_PREFILL && phase != EXFOLD_PHASE_DECODE)
+    return EXFOLD_ERR_ARG;
+  st = check_routing(T, L->n_experts, L->top_k);
+  if (st != EXFOLD_OK) return st;
+  if (phase != EXFOLD_PHASE_DENSE && budget < 1) return EXFOLD_ERR_BUDGET;
+  p.T = (int)T;
+  p.N = (int)L->n_experts;
+  p.K = (int)L->top_k;
+  p.phase = phase;
+  p.budget = (int)(budget > (1 << 20) ? (1 << 20) : budget);
+  p.k_out = (phase == EXFOLD_PHASE_PREFILL) ? (p.budget < p.K ? p.budget : p.K) : p.K;
+  p.dcap = (p.budget < p.N) ? p.budget : p.N;
+  Carver c;
+  p.o_logits = c.take(sizeof(float) * (size_t)p.T * p.N);
+  p.o_topk_ids = c.take(sizeof(int32_t) * (size_t)p.T * p.K);
+  p.o_topk_w = c.take(sizeof(float) * (size_t)p.T * p.K);
+  p.o_keep = c.take((size_t)p.T * p.K);
+  p.o_pool = c.take(sizeof(int32_t) * p.N);
+  p.o_pool_size = c.take(sizeof(int32_t));
+  p.o_tgt = c.take(sizeof(int32_t) * p.N);
+  p.o_scl = c.take(sizeof(float) * p.N);
+  p.o_fold_ids = c.take(sizeof(int32_t) * (size_t)p.T * p.k_out);
+  p.o_fold_w = c.take(sizeof(float) * (size_t)p.T * p.k_out);
+  int active = p.N;
+  if (phase == EXFOLD_PHASE_DECODE) active = p.dcap;
+  if (p.T * p.k_out < active) active = p.T * p.k_out;
+  if (L->shared_inter > 0) active += 1;
+  plan_exec(L, phase, p.T, p.k_out, true, false, active, c, p.ex);
+  p.total = c.off;
+  return EXFOLD_OK;
+}
+
+exfold_status plan_execute(const exfold_layer *L, int64_t T, int64_t k_out, ExecPlan &p,
+                           size_t &total) {
+  exfold_status st = check_layer(L);
+  if (st != EXFOLD_OK) return st;
+  if (k_out < 1 || k_out > kMaxExperts * 4) return EXFOLD_ERR_SHAPE;
+  if (T < 0 || T > kMaxTokens || T * k_out > kMaxSlots) return EXFOLD_ERR_SHAPE;
+  Carver c;
+  int active = (int)L->n_experts;
+  if (T * k_out < active) active = (int)(T * k_out);
+  if (L->shared_inter > 0) active += 1;
+  plan_exec(L, EXFOLD_PHASE_DENSE, (int)T, (int)k_out, true, false, active, c, p);
+  total = c.off;
+  return EXFOLD_OK;
+}
+
+struct CalibPlan {
+  int m = 0, N = 0, K = 0, kr = 0;
+  size_t o_logits = 0, o_topk_ids = 0, o_topk_w = 0, o_route_ids = 0, o_route_w = 0, o_pos = 0,
+         o_gram = 0;
+  ExecPlan ex;
+  size_t total = 0;
+};
+
+exfold_status plan_calibrate(const exfold_layer *L, int64_t m, int32_t mode, CalibPlan &p) {
+  exfold_status st = check_layer(L);
+  if (st != EXFOLD_OK) return st;
+  if (mode != EXFOLD_CAL_COROUTED && mode != EXFOLD_CAL_COMMON) return EXFOLD_ERR_ARG;
+  st = check_routing(m, L->n_experts, L->top_k);
+  if (st != EXFOLD_OK) return st;
+  p.m = (int)m;
+  p.N = (int)L->n_experts;
+  p.K = (int)L->top_k;
+  p.kr = (mode == EXFOLD_CAL_COMMON) ? p.N : p.K;
+  if ((int64_t)p.m * p.kr > kMaxSlots) return EXFOLD_ERR_SHAPE;
+  Carver c;
+  p.o_logits = c.take(sizeof(float) * (size_t)p.m * p.N);
+  p.o_topk_ids = c.take(sizeof(int32_t) * (size_t)p.m * p.K);
+  p.o_topk_w = c.take(sizeof(float) * (size_t)p.m * p.K);
+  p.o_route_ids = c.take(sizeof(int32_t) * (size_t)p.m * p.kr);
+  p.o_route_w = c.take(sizeof(float) * (size_t)p.m * p.kr);
+  p.o_pos = c.take(sizeof(int16_t) * (size_t)p.m * p.N);
+  p.o_gram = c.take(sizeof(double) * (size_t)p.m * p.kr * p.kr);
+  plan_exec(L, EXFOLD_PHASE_PREFILL, p.m, p.kr, false, true, p.N, c, p.ex);
+  p.total = c.off;
+  return EXFOLD_OK;
+}
+
+exfold_status check_ws(void *ws, size_t ws_bytes, size_t need) {
+  if (need > 0 && !ws) return EXFOLD_ERR_NULL;
+  if (ws_bytes < need) return EXFOLD_ERR_WORKSPACE;
+  if (reinterpret_cast<uintptr_t>(ws) % kAlign != 0) return EXFOLD_ERR_WORKSPACE;
+  return EXFOLD_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *exfold_status_str(exfold_status s) {
+  switch (s) {
+    case EXFOLD_OK: return "ok";
+    case EXFOLD_ERR_NULL: return "required pointer is NULL";
+    case EXFOLD_ERR_SHAPE: return "size out of range or inconsistent";
+    case EXFOLD_ERR_BUDGET: return "budget must be >= 1";
+    case EXFOLD_ERR_DTYPE: return "unknown dtype";
+    case EXFOLD_ERR_WORKSPACE: return "workspace too small or misaligned";
+    case EXFOLD_ERR_DEVICE: return "HIP launch failed";
+    case EXFOLD_ERR_UNSUPPORTED: return "outside the kernels' limits";
+    case EXFOLD_ERR_ARG: return "invalid phase, mode or scalar argument";
+    default: return "unknown status";
+  }
+}
+
+exfold_status exfold_select_prefill(const float *logits, int64_t T, int64_t N, int64_t K,
+                                    int64_t k_pre, const float *h, int32_t *topk_ids,
+                                    float *topk_w, uint8_t *keep, void *stream) {
+  exfold_status st = check_routing(T, N, K);
+  if (st != EXFOLD_OK) return st;
+  if (k_pre < 1) return EXFOLD_ERR_BUDGET;
+  if (T == 0) return EXFOLD_OK;
+  if (!h || !topk_ids || !topk_w || !keep) return EXFOLD_ERR_NULL;
+  const int kp = (int)(k_pre > K ? K : k_pre);
+  if (launch_route_tokens(logits, (int)T, (int)N, (int)K, kp, h, nullptr, nullptr, topk_ids, topk_w,
+                          keep, nullptr, nullptr, nullptr, static_cast<hipStream_t>(stream)) != hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  return EXFOLD_OK;
+}
+
+exfold_status exfold_select_decode_pool(const float *logits, int64_t B, int64_t N, int64_t K,
+                                        int64_t D, const float *h, int32_t *topk_ids,
+                                        float *topk_w, int32_t *pool, int32_t *pool_size,
+                                        void *stream) {
+  exfold_status st = check_routing(B, N, K);
+  if (st != EXFOLD_OK) return st;
+  if (D < 1) return EXFOLD_ERR_BUDGET;
+  if (!h || !pool || !pool_size) return EXFOLD_ERR_NULL;
+  if (B > 0 && (!topk_ids || !topk_w)) return EXFOLD_ERR_NULL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int dd = (int)(D > N ? N : D);
+  if (logits && B > 0) {
+    if (launch_route_tokens(logits, (int)B, (int)N, (int)K, (int)K, nullptr, nullptr, nullptr,
+                            topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+  }
+  if (launch_decode_pool_fold(topk_ids, topk_w, (int)B, (int)N, (int)K, dd, h, nullptr, nullptr,
+                              true, pool, pool_size, nullptr, nullptr, nullptr, nullptr,
+                              s) != hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  return EXFOLD_OK;
+}
+
+exfold_status exfold_fold_gates(int32_t phase, int64_t T, int64_t N, int64_t K, int64_t budget,
+                                const int32_t *topk_ids, const float *topk_w,
+                                const uint8_t *keep, const int32_t *pool,
+                                const int32_t *pool_size, const float *S, const float *L,
+                                int32_t *out_ids, float *out_w, int32_t *tgt_ids,
+                                float *tgt_scale, void *stream) {
+  if (phase != EXFOLD_PHASE_PREFILL && phase != EXFOLD_PHASE_DECODE) return EXFOLD_ERR_ARG;
+  exfold_status st = check_routing(T, N, K);
+  if (st != EXFOLD_OK) return st;
+  if (budget < 1) return EXFOLD_ERR_BUDGET;
+  if (!S || !L) return EXFOLD_ERR_NULL;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (phase == EXFOLD_PHASE_PREFILL) {
+    if (T == 0) return EXFOLD_OK;
+    if (!topk_ids || !topk_w || !keep || !out_ids || !out_w) return EXFOLD_ERR_NULL;
+    const int kp = (int)(budget > K ? K : budget);
+    if (launch_route_tokens(nullptr, (int)T, (int)N, (int)K, kp, nullptr, S, L,
+                            const_cast<int32_t *>(topk_ids), const_cast<float *>(topk_w), nullptr,
+                            keep, out_ids, out_w, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+    return EXFOLD_OK;
+  }
+  if (!pool || !pool_size) return EXFOLD_ERR_NULL;
+  if (T > 0 && (!topk_ids || !topk_w || !out_ids || !out_w)) return EXFOLD_ERR_NULL;
+  if (T == 0 && !tgt_ids && !tgt_scale) return EXFOLD_OK;
+  const int dd = (int)(budget > N ? N : budget);
+  if (launch_decode_pool_fold(topk_ids, topk_w, (int)T, (int)N, (int)K, dd, nullptr, S, L, false,
+                              const_cast<int32_t *>(pool), const_cast<int32_t *>(pool_size),
+                              T > 0 ? out_ids : nullptr, T > 0 ? out_w : nullptr, tgt_ids,
+                              tgt_scale, s) != hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  return EXFOLD_OK;
+}
+
+size_t exfold_moe_workspace_size(const exfold_layer *layer, int64_t T, int32_t phase,
+                                 int64_t budget) {
+  ForwardPlan p;
+  if (plan_forward(layer, T, phase, budget, p) != EXFOLD_OK) return 0;
+  return p.total;
+}
+
+exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables *tables,
+                                 const void *x, int64_t T, int32_t phase, int64_t budget,
+                                 void *y, const exfold_debug *debug, void *ws, size_t ws_bytes,
+                                 void *stream) {
+  ForwardPlan p;
+  exfold_status st = plan_forward(layer, T, phase, budget, p);
+  if (st != EXFOLD_OK) return st;
+  if (phase != EXFOLD_PHASE_DENSE && (!tables || !tables->S || !tables->L || !tables->h))
+    return EXFOLD_ERR_NULL;
+  if (T == 0) return EXFOLD_OK;
+  if (!x || !y) return EXFOLD_ERR_NULL;
+  st = check_ws(ws, ws_bytes, p.total);
+  if (st != EXFOLD_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const exfold_debug z{};
+  const exfold_debug &dbg = debug ? *debug : z;
+  float *logits = dbg.logits ? dbg.logits : at<float>(ws, p.o_logits);
+  int32_t *topk_ids = dbg.topk_ids ? dbg.topk_ids : at<int32_t>(ws, p.o_topk_ids);
+  float *topk_w = dbg.topk_w ? dbg.topk_w : at<float>(ws, p.o_topk_w);
+  uint8_t *keep = dbg.keep ? dbg.keep : at<uint8_t>(ws, p.o_keep);
+  int32_t *pool = dbg.pool ? dbg.pool : at<int32_t>(ws, p.o_pool);
+  int32_t *pool_size = dbg.pool_size ? dbg.pool_size : at<int32_t>(ws, p.o_pool_size);
+  int32_t *fold_ids = dbg.fold_ids ? dbg.fold_ids : at<int32_t>(ws, p.o_fold_ids);
+  float *fold_w = dbg.fold_w ? dbg.fold_w : at<float>(ws, p.o_fold_w);
+
+  record(dbg.events, EXFOLD_EV_START, s);
+  if (launch_router_logits(layer->dtype, x, layer->w_router, layer->router_bias, p.T, p.N,
+                           (int)layer->d, logits, s) != hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  record(dbg.events, EXFOLD_EV_ROUTER, s);
+  const int32_t *exec_ids = fold_ids;
+  const float *exec_w = fold_w;
+  hipError_t e = hipSuccess;
+  if (phase == EXFOLD_PHASE_DENSE) {
+    e = launch_route_tokens(logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr, topk_ids, topk_w,
+                            nullptr, nullptr, nullptr, nullptr, s);
+    exec_ids = topk_ids;
+    exec_w = topk_w;
+  } else if (phase == EXFOLD_PHASE_PREFILL) {
+    e = launch_route_tokens(logits, p.T, p.N, p.K, p.k_out, tables->h, tables->S, tables->L,
+                            topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s);
+  } else {
+    e = launch_route_tokens(logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr, topk_ids, topk_w,
+                            nullptr, nullptr, nullptr, nullptr, s);
+    if (e == hipSuccess)
+      e = launch_decode_pool_fold(topk_ids, topk_w, p.T, p.N, p.K, p.dcap, tables->h, tables->S,
+                                  tables->L, true, pool, pool_size, fold_ids, fold_w, dbg.tgt_ids,
+                                  dbg.tgt_scale, s);
+  }
+  if (e != hipSuccess) return EXFOLD_ERR_DEVICE;
+  record(dbg.events, EXFOLD_EV_FOLD, s);
+  return run_exec(layer, p.ex, x, exec_ids, exec_w, y, ws, dbg.offsets, dbg.row_slot, false, s,
+                  dbg.events);
+}
+
+size_t exfold_execute_workspace_size(const exfold_layer *layer, int64_t T, int64_t k_out) {
+  ExecPlan p;
+  size_t total = 0;
+  if (plan_execute(layer, T, k_out, p, total) != EXFOLD_OK) return 0;
+  return total;
+}
+
+exfold_status exfold_moe_execute(const exfold_layer *layer, const void *x, int64_t T,
+                                 int64_t k_out, const int32_t *route_ids, const float *route_w,
+                                 void *y, const exfold_debug *debug, void *ws, size_t ws_bytes,
+                                 void *stream) {
+  ExecPlan p;
+  size_t total = 0;
+  exfold_status st = plan_execute(layer, T, k_out, p, total);
+  if (st != EXFOLD_OK) return st;
+  if (T == 0) return EXFOLD_OK;
+  if (!x || !y || !route_ids || !route_w) return EXFOLD_ERR_NULL;
+  st = check_ws(ws, ws_bytes, total);
+  if (st != EXFOLD_OK) return st;
+  return run_exec(layer, p, x, route_ids, route_w, y, ws, debug ? debug->offsets : nullptr,
+                  debug ? debug->row_slot : nullptr, false, static_cast<hipStream_t>(stream));
+}
+
+size_t exfold_calibrate_workspace_size(const exfold_layer *layer, int64_t m, int32_t mode) {
+  CalibPlan p;
+  if (plan_calibrate(layer, m, mode, p) != EXFOLD_OK) return 0;
+  return p.total;
+}
+
+exfold_status exfold_calibrate_projectors(const exfold_layer *layer, const void *x_cal, int64_t m,
+                                          double lambda, double clip, int32_t mode, float *S,
+                                          float *L, float *h, double *pair_stats, void *ws,
+                                          size_t ws_bytes, void *stream) {
+  CalibPlan p;
+  exfold_status st = plan_calibrate(layer, m, mode, p);
+  if (st != EXFOLD_OK) return st;
+  if (!(lambda >= 0.0) || !(clip >= 0.0)) return EXFOLD_ERR_ARG;
+  if (!S || !L || !h) return EXFOLD_ERR_NULL;
+  if (m > 0 && !x_cal) return EXFOLD_ERR_NULL;
+  st = check_ws(ws, ws_bytes, p.total);
+  if (st != EXFOLD_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float *logits = at<float>(ws, p.o_logits);
+  int32_t *topk_ids = at<int32_t>(ws, p.o_topk_ids);
+  float *topk_w = at<float>(ws, p.o_topk_w);
+  int32_t *route_ids = at<int32_t>(ws, p.o_route_ids);
+  float *route_w = at<float>(ws, p.o_route_w);
+  int16_t *pos = at<int16_t>(ws, p.o_pos);
+  double *gram = at<double>(ws, p.o_gram);
+  if (p.m > 0) {
+    if (launch_router_logits(layer->dtype, x_cal, layer->w_router, layer->router_bias, p.m, p.N,
+                             (int)layer->d, logits, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+    if (launch_route_tokens(logits, p.m, p.N, p.K, p.K, nullptr, nullptr, nullptr, topk_ids, topk_w,
+                            nullptr, nullptr, nullptr, nullptr, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+    if (launch_calib_routes(topk_ids, p.m, p.N, p.K, mode, route_ids, route_w, pos, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+    st = run_exec(layer, p.ex, x_cal, route_ids, route_w, nullptr, ws, nullptr, nullptr, true, s);
+    if (st != EXFOLD_OK) return st;
+    if (launch_calib_gram(at<float>(ws, p.ex.o_Y), at<int32_t>(ws, p.ex.o_slot_row), p.m, p.kr,
+                          (int)layer->d, gram, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+  }
+  if (launch_calib_finalize(gram, pos, p.m, p.N, p.kr, lambda, clip, S, L, h, pair_stats, s) !=
+      hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  return EXFOLD_OK;
+}
+
+}  // extern "C"

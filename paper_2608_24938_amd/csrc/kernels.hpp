@@ -1,0 +1,80 @@
+// Internal launchers of the libexfold kernels.  Every launcher enqueues on
+// `stream` and returns hipGetLastError() of its launches.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace exfold {
+
+// ---- routing (k_route.hip) ----
+hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, const float *bias,
+                                int T, int N, int d, float *logits, hipStream_t s);
+// Per-token Top-K + softmax (if logits != nullptr), prefill selection (if keep
+// or fold outputs are requested) and prefill fold (if fold_ids != nullptr).
+hipError_t launch_route_tokens(const float *logits, int T, int N, int K, int k_pre, const float *h,
+                               const float *S, const float *L, int32_t *topk_ids, float *topk_w,
+                               uint8_t *keep, const uint8_t *keep_in, int32_t *fold_ids,
+                               float *fold_w, hipStream_t s);
+// Decode pool (if do_pool) and per-source tables + per-slot remap (if out_ids).
+hipError_t launch_decode_pool_fold(const int32_t *ids, const float *w, int B, int N, int K, int D,
+                                   const float *h, const float *S, const float *L, bool do_pool,
+                                   int32_t *pool, int32_t *pool_size, int32_t *out_ids,
+                                   float *out_w, int32_t *tgt, float *scl, hipStream_t s);
+
+// ---- permutation (k_permute.hip) ----
+constexpr int kPermSlotsPerBlock = 1024;
+struct PermBuffers {
+  int32_t *blk_counts;   // [nblk, N]
+  int32_t *offsets;      // [N + 2]: routed groups, then the shared group
+  int32_t *tile_start0;  // [N + 2]: m-tile prefix for tile height bm0
+  int32_t *tile_start1;  // [N + 2]: m-tile prefix for tile height bm1
+  int32_t *row_token;    // [R + T_shared]
+  int32_t *row_slot;     // [R + T_shared] (-1 for shared rows)
+  float *row_w;          // [R + T_shared]
+  int32_t *slot_row;     // [R]
+};
+// Stable counting sort of R = T*k_out route slots by expert; the T_shared
+// shared-expert rows are appended after the routed rows.
+hipError_t launch_permute(const int32_t *route_ids, const float *route_w, int T, int k_out, int N,
+                          int t_shared, int bm0, int bm1, const PermBuffers &pb, hipStream_t s);
+
+// ---- expert GEMMs and combine (k_gemm.hip) ----
+struct GemmPlan {
+  int bm, bn, ksplit;
+  int grid;
+};
+struct ExpertArgs {
+  int dtype;
+  int d, inter, n_experts, groups;  // groups = N (+1 with a shared expert)
+  const void *x;                     // [T, d]
+  const void *w_gate_up, *w_down;    // routed [N, 2I, d], [N, d, I]
+  const void *ws_gate_up, *ws_down;  // shared or nullptr
+  const int32_t *offsets, *tile_start_gu, *tile_start_dn;
+  const int32_t *row_token;
+  const float *row_w;
+  int rows;     // R + T_shared
+  void *H;      // [rows, I]
+  float *Y;     // [ksplit, rows, d] partial outputs (nullptr when direct)
+  void *y;      // [T, d] direct output (each token owns exactly one row)
+  bool direct;
+};
+// active_groups: expected number of non-empty groups (sizes the down split).
+void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d, int inter,
+                       int cu_count, GemmPlan *gate_up, GemmPlan *down);
+// ev_mid (optional) is recorded between the gate_up and the down GEMM.
+hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const GemmPlan &dn,
+                               hipStream_t s, hipEvent_t ev_mid = nullptr);
+hipError_t launch_combine(int dtype, const float *Y, int ksplit, int rows, const int32_t *slot_row,
+                          int T, int k_out, int d, int shared_base, void *y, hipStream_t s);
+
+// ---- calibration (k_calib.hip) ----
+hipError_t launch_calib_routes(const int32_t *topk_ids, int m, int N, int K, int mode,
+                               int32_t *route_ids, float *route_w, int16_t *pos, hipStream_t s);
+hipError_t launch_calib_gram(const float *Y, const int32_t *slot_row, int m, int kr, int d,
+                             double *gram, hipStream_t s);
+hipError_t launch_calib_finalize(const double *gram, const int16_t *pos, int m, int N, int kr,
+                                 double lambda, double clip, float *S, float *L, float *h,
+                                 double *pair_stats, hipStream_t s);
+
+}  // namespace exfold

@@ -174,3 +174,15 @@ def all_expert_weights(shape: LayerShape, seed: int = 0, threads: int = 8):
     with ThreadPoolExecutor(max_workers=threads) as ex:
         list(ex.map(job, [(e, p) for e in range(shape.n_experts) for p in (0, 1)]))
     return gu, dn
+
+
+def synthetic_tables(n_experts: int, seed: int = 0):
+    """Seeded stand-in projector tables (S, L [N, N], h [N], float32) for speed and parity runs:
+    S ~ N(0, 0.5^2), L ~ U(0, 1) with a zero diagonal and S = 1 on it, h ~ U(0.5, 2)."""
+    rng = _rng(16 * seed + 4)
+    S = (rng.standard_normal((n_experts, n_experts), dtype=np.float32) * np.float32(0.5))
+    L = rng.random((n_experts, n_experts), dtype=np.float32)
+    np.fill_diagonal(S, 1.0)
+    np.fill_diagonal(L, 0.0)
+    h = (np.float32(0.5) + np.float32(1.5) * rng.random(n_experts, dtype=np.float32)).astype(np.float32)
+    return S, L, h

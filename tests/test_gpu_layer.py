@@ -1,0 +1,218 @@
+"""Layer-level parity of the HIP path with the oracle: expert execution on
+given routes, the full folded forward in every phase, the identity budgets,
+exact-multiple folding, calibration and determinism."""
+
+import numpy as np
+import pytest
+import torch
+
+from oracle import exfold_oracle as O
+from paper_2608_24938_amd import exfold as X
+from paper_2608_24938_amd import synth
+
+from .gpu_common import (DEV, TOL_Y, LayerPair, from_dev, logits_bound, per_token_rel_l2, sync, to_dev,
+                         topk_near_tie)
+
+pytestmark = pytest.mark.gpu
+
+SMALL_BF16 = synth.LayerShape("small-bf16", d=256, inter=512, n_experts=8, top_k=2, dtype="bf16", m_cal=512)
+WIDE_BF16 = synth.LayerShape("wide-bf16", d=256, inter=128, n_experts=128, top_k=8, dtype="bf16",
+                             router_bias=True, m_cal=1024)
+SHARED_BF16 = synth.LayerShape("shared-bf16", d=384, inter=192, n_experts=64, top_k=6, shared_inter=192,
+                               dtype="bf16", m_cal=512)
+WIDE_F32 = synth.LayerShape("wide-f32", d=128, inter=64, n_experts=64, top_k=8, dtype="f32", router_bias=True)
+
+
+@pytest.mark.parametrize("shape,T,k_out", [(synth.TINY, 64, 2), (synth.TINY, 1, 1), (SMALL_BF16, 200, 2),
+                                           (WIDE_BF16, 300, 8), (SHARED_BF16, 77, 3), (WIDE_F32, 150, 5),
+                                           (SMALL_BF16, 513, 1)])
+def test_execute_matches_oracle(shape, T, k_out):
+    lp = LayerPair(shape, seed=1)
+    rng = np.random.default_rng(T)
+    ids = rng.integers(0, shape.n_experts, size=(T, k_out)).astype(np.int32)   # duplicates allowed
+    w = rng.standard_normal((T, k_out)).astype(np.float32)
+    xs = synth.tokens(shape, T, seed=1)
+    y = X.moe_execute(lp.dev, to_dev(xs), to_dev(ids), to_dev(w))
+    sync()
+    ref = O.moe_output(lp.ref, synth.widen(xs), ids, w)
+    err = per_token_rel_l2(from_dev(y), ref)
+    assert err.max() <= TOL_Y[shape.dtype], err.max()
+
+
+def _forward_case(shape, T, phase, budget, seed=2):
+    lp = LayerPair(shape, seed=seed)
+    xs = synth.tokens(shape, T, seed=seed)
+    S, L, h = synth.synthetic_tables(shape.n_experts, seed=seed)
+    dbg = X.debug_buffers(lp.dev, T, phase, budget, DEV)
+    y = X.moe_forward(lp.dev, to_dev(xs), phase, budget, to_dev(S), to_dev(L), to_dev(h), debug=dbg)
+    sync()
+    return lp, xs, (S, L, h), dbg, from_dev(y)
+
+
+@pytest.mark.parametrize("shape,T,phase,budget", [
+    (synth.TINY, 64, "prefill", 1), (synth.TINY, 64, "dense", 0), (synth.TINY, 64, "decode", 4),
+    (SMALL_BF16, 300, "prefill", 1), (SMALL_BF16, 32, "decode", 4), (SMALL_BF16, 129, "dense", 0),
+    (WIDE_BF16, 500, "prefill", 4), (WIDE_BF16, 64, "decode", 16), (WIDE_BF16, 256, "decode", 32),
+    (SHARED_BF16, 100, "prefill", 2), (SHARED_BF16, 48, "decode", 8), (WIDE_F32, 90, "prefill", 3),
+    (WIDE_F32, 33, "decode", 5),
+])
+def test_forward_matches_oracle(shape, T, phase, budget):
+    lp, xs, (S, L, h), dbg, y = _forward_case(shape, T, phase, budget)
+    x = synth.widen(xs)
+    # router logits within the float32 rounding bound
+    ref_logits = O.router_logits(x, lp.ref.w_router, lp.ref.router_bias)
+    bound = logits_bound(x, lp.ref.w_router, lp.ref.router_bias, shape.d)
+    g_logits = dbg["logits"].cpu().numpy().astype(np.float64)
+    assert np.all(np.abs(g_logits - ref_logits) <= bound)
+    # oracle forward from x (its own float64 routing)
+    y_ref, info = O.moe_forward(lp.ref, x, shape.top_k, phase, budget, S, L, h)
+    tie = topk_near_tie(ref_logits, bound, shape.top_k)
+    g_ids = dbg["topk_ids"].cpu().numpy()
+    same_routes = np.all(g_ids == info["topk_ids"], axis=1)
+    assert np.all(same_routes | tie), "route mismatch away from a near-tie"
+    ok = same_routes.copy()
+    if phase == "prefill":
+        same_fold = np.all(dbg["fold_ids"].cpu().numpy() == info["fold_ids"], axis=1)
+        ok &= same_fold
+        assert same_fold[same_routes].mean() >= 0.99
+    elif phase == "decode":
+        n = int(dbg["pool_size"].item())
+        assert n == len(info["pool"])
+        g_pool = dbg["pool"].cpu().numpy()[:n].tolist()
+        if g_pool != info["pool"]:
+            # only a near-tie of the batch scores may reorder the pool: check the margin
+            w = info["topk_w"].astype(np.float64)
+            score = np.zeros(shape.n_experts)
+            np.add.at(score, info["topk_ids"].reshape(-1), w.reshape(-1))
+            score *= h.astype(np.float64)
+            diff = sorted(set(g_pool) ^ set(info["pool"]))
+            assert np.ptp(score[diff]) <= 1e-5 * score.max(), "pool differs away from a near-tie"
+            ok &= ~np.isin(info["topk_ids"], diff).any(axis=1)
+        np.testing.assert_array_equal(dbg["fold_ids"].cpu().numpy()[ok], info["fold_ids"][ok])
+    assert ok.mean() >= 0.9, ok.mean()
+    err = per_token_rel_l2(y, y_ref)[ok]
+    assert err.max() <= TOL_Y[shape.dtype], err.max()
+
+
+@pytest.mark.parametrize("shape,T,K_id,D_id", [(WIDE_F32, 64, 8, 64), (WIDE_BF16, 200, 8, 128),
+                                              (SHARED_BF16, 60, 6, 64)])
+def test_identity_budgets_are_bitwise_dense(shape, T, K_id, D_id):
+    lp = LayerPair(shape, seed=4)
+    xs = to_dev(synth.tokens(shape, T, seed=4))
+    S, L, h = (to_dev(a) for a in synth.synthetic_tables(shape.n_experts, seed=4))
+    y0 = X.moe_forward(lp.dev, xs, "dense", 0)
+    yp = X.moe_forward(lp.dev, xs, "prefill", K_id, S, L, h)
+    yp2 = X.moe_forward(lp.dev, xs, "prefill", K_id + 5, S, L, h)
+    yd = X.moe_forward(lp.dev, xs, "decode", D_id, S, L, h)
+    # |candidates| <= D < N: the routes are bitwise unchanged (y then agrees within tolerance:
+    # the expert GEMMs are planned for a pool of D, so the sums may be split differently)
+    x3 = xs[:3].contiguous()
+    y3 = X.moe_forward(lp.dev, x3, "dense", 0)
+    dbg = X.debug_buffers(lp.dev, 3, "decode", D_id - 1, DEV)
+    yd3 = X.moe_forward(lp.dev, x3, "decode", D_id - 1, S, L, h, debug=dbg)
+    sync()
+    bits = lambda y: y.view(torch.int16) if y.dtype == torch.bfloat16 else y.view(torch.int32)
+    for y in (yp, yp2, yd):
+        assert torch.equal(bits(y), bits(y0))
+    assert int(dbg["pool_size"].item()) <= 3 * shape.top_k < D_id - 1
+    assert torch.equal(dbg["fold_ids"], dbg["topk_ids"])
+    assert torch.equal(dbg["fold_w"].view(torch.int32), dbg["topk_w"].view(torch.int32))
+    err = per_token_rel_l2(from_dev(yd3), from_dev(y3).astype(np.float64))
+    assert err.max() <= TOL_Y[shape.dtype]
+
+
+def _twin_layer(dtype, seed=5):
+    """Experts 4+j copy gate/up of expert j and scale its down projection by c_j (a power of two);
+    the router ranks every base expert just above its twin."""
+    c = (0.5, -2.0, 2.0, -0.5)   # no c = -1: twin logits differ by 1e-4, so E_j - E_tw would cancel
+    shape = synth.LayerShape("twin", d=256, inter=128, n_experts=8, top_k=2, dtype=dtype)
+    lp = LayerPair(shape, seed=seed)
+    gu, dn, wr = lp.storage["gu"].copy(), lp.storage["dn"].copy(), lp.storage["wr"].copy()
+    gu[4:] = gu[:4]
+    wr[4:] = wr[:4]
+    scaled = synth.widen(dn[:4]) * np.array(c, np.float32)[:, None, None]
+    dn[4:] = synth._bf16_bits_inplace(scaled.copy()) if dtype == "bf16" else scaled
+    bias = np.array([0, 0, 0, 0, -1e-4, -1e-4, -1e-4, -1e-4], np.float32)
+    dev = X.Layer(w_router=to_dev(wr), w_gate_up=to_dev(gu), w_down=to_dev(dn), top_k=2, router_bias=to_dev(bias))
+    ref = O.Layer(w_router=synth.widen(wr), w_gate_up=synth.widen(gu), w_down=synth.widen(dn), router_bias=bias)
+    return shape, dev, ref, c
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_exact_multiples_fold_reproduces_full_output(dtype):
+    shape, dev, ref, c = _twin_layer(dtype)
+    xc = to_dev(synth.calibration_tokens(shape, 256, seed=5))
+    S, L, h = X.calibrate_projectors(dev, xc, lam=0.0, clip=4.0, mode="common")
+    sync()
+    S_, L_ = S.cpu().numpy(), L.cpu().numpy()
+    for j, cj in enumerate(c):
+        if dtype == "f32":
+            # float32 experts: u = c v holds bit for bit, so s = c and l = 0 exactly
+            assert S_[4 + j, j] == np.float32(cj) and S_[j, 4 + j] == np.float32(1.0 / cj)
+            assert L_[4 + j, j] == 0.0 and L_[j, 4 + j] == 0.0
+        else:
+            # bf16 MFMA products: the scaled twin agrees to the last float32 bits
+            assert abs(S_[4 + j, j] - cj) <= 1e-6 * abs(cj) and abs(S_[j, 4 + j] - 1 / cj) <= 1e-6 / abs(cj)
+            assert L_[4 + j, j] <= 1e-6 and L_[j, 4 + j] <= 1e-6
+    T = 96
+    xs = synth.tokens(shape, T, seed=6)
+    x = to_dev(xs)
+    y_full = O.moe_forward(ref, synth.widen(xs), 2, "dense", 0)[0]
+    dbg = X.debug_buffers(dev, T, "prefill", 1, DEV)
+    yp = X.moe_forward(dev, x, "prefill", 1, S, L, h, debug=dbg)
+    hd = to_dev(np.array([10, 10, 10, 10, 1, 1, 1, 1], np.float32))
+    dbgd = X.debug_buffers(dev, T, "decode", 4, DEV)
+    yd = X.moe_forward(dev, x, "decode", 4, S, L, hd, debug=dbgd)
+    sync()
+    ids = dbg["topk_ids"].cpu().numpy()
+    twin = (ids[:, 0] % 4) == (ids[:, 1] % 4)
+    assert twin.mean() > 0.95
+    assert sorted(dbgd["pool"].cpu().numpy().tolist()) == [0, 1, 2, 3]
+    for y in (yp, yd):
+        err = per_token_rel_l2(from_dev(y), y_full)[twin]
+        assert err.max() <= TOL_Y[dtype], err.max()
+
+
+@pytest.mark.parametrize("shape,m,mode,lam,clip", [(synth.TINY, 512, "corouted", 1e-3, 4.0),
+                                                   (synth.TINY, 200, "common", 1e-3, 0.0),
+                                                   (WIDE_F32, 300, "corouted", 1e-2, 4.0),
+                                                   (SMALL_BF16, 512, "corouted", 1e-3, 4.0)])
+def test_calibration_matches_oracle(shape, m, mode, lam, clip):
+    lp = LayerPair(shape, seed=7)
+    xs = synth.calibration_tokens(shape, m, seed=7)
+    S, L, h, st = X.calibrate_projectors(lp.dev, to_dev(xs), lam=lam, clip=clip, mode=mode, with_stats=True)
+    sync()
+    rS, rL, rh, rst = O.calibrate(lp.ref, synth.widen(xs), shape.top_k, lam=lam, clip=clip, mode=mode)
+    st = st.cpu().numpy()
+    np.testing.assert_array_equal(st[..., 3], rst["n"])
+    tol = 1e-4 if shape.dtype == "f32" else 2e-2
+    obs = rst["n"] > 0
+    np.testing.assert_allclose(st[..., 0][obs], rst["A"][obs], rtol=tol, atol=tol * np.abs(rst["A"]).max())
+    np.testing.assert_allclose(st[..., 1][obs], rst["V"][obs], rtol=tol)
+    np.testing.assert_allclose(st[..., 2][obs], rst["C"][obs], rtol=tol)
+    S, L, h = S.cpu().numpy(), L.cpu().numpy(), h.cpu().numpy()
+    np.testing.assert_allclose(S, rS, rtol=tol, atol=tol * max(1.0, np.abs(rS).max()))
+    np.testing.assert_array_equal(L[~obs], rL[~obs])                  # 1e30 and the zero diagonal exactly
+    np.testing.assert_allclose(L[obs], rL[obs], rtol=tol, atol=tol)
+    np.testing.assert_allclose(h, rh, rtol=tol)
+
+
+@pytest.mark.parametrize("shape,T,phase,budget", [(WIDE_BF16, 700, "prefill", 4), (WIDE_BF16, 64, "decode", 16),
+                                                  (SHARED_BF16, 100, "decode", 8)])
+def test_forward_is_deterministic(shape, T, phase, budget):
+    lp = LayerPair(shape, seed=8)
+    xs = to_dev(synth.tokens(shape, T, seed=8))
+    S, L, h = (to_dev(a) for a in synth.synthetic_tables(shape.n_experts, seed=8))
+    a = X.moe_forward(lp.dev, xs, phase, budget, S, L, h)
+    b = X.moe_forward(lp.dev, xs, phase, budget, S, L, h)
+    sync()
+    assert torch.equal(a.view(torch.int16), b.view(torch.int16))
+
+
+def test_zero_tokens_is_a_noop():
+    lp = LayerPair(synth.TINY, seed=9)
+    x = torch.empty((0, 256), dtype=torch.float32, device=DEV)
+    S, L, h = (to_dev(a) for a in synth.synthetic_tables(8, seed=9))
+    y = X.moe_forward(lp.dev, x, "prefill", 1, S, L, h)
+    sync()
+    assert y.shape == (0, 256)
