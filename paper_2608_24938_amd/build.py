@@ -27,6 +27,8 @@ FLAGS = [
     f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-Wall",
     "-Wno-unused-function", "-Wno-unused-variable",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # keep per-thread address arrays in registers (the pass would move them to LDS)
+    "-mllvm", "-disable-promote-alloca-to-lds",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
 SOURCES = ["exfold_api.hip", "k_route.hip", "k_permute.hip", "k_gemm.hip", "k_calib.hip"]

@@ -17,6 +17,9 @@ typedef uint16_t bf16_t;  // raw bf16 storage
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
+// 16-byte staging register (a native vector: HIP's uint4 is a union-based
+// struct that the optimiser cannot keep in registers when held in arrays)
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 

@@ -94,8 +94,6 @@ void plan_exec(const exfold_layer *L, int phase, int T, int k_out, bool with_sha
   (void)phase;
   plan_expert_gemms(p.dtype, p.rows, p.groups, active_groups, p.d, p.inter, cu_count(), &p.gu,
                     &p.dn);
-  if (p.direct || keep_rows) p.dn.ksplit = 1, p.dn.grid = (p.rows / p.dn.bm + p.groups) * (p.d / p.dn.bn);
-  if (p.dtype != EXFOLD_BF16) p.dn.ksplit = 1;
   const int nblk = (p.R + kPermSlotsPerBlock - 1) / kPermSlotsPerBlock;
   const size_t esz = (p.dtype == EXFOLD_BF16) ? 2 : 4;
   p.o_blk = c.take(sizeof(int32_t) * (size_t)(nblk > 0 ? nblk : 1) * p.N);
@@ -107,6 +105,10 @@ void plan_exec(const exfold_layer *L, int phase, int T, int k_out, bool with_sha
   p.o_row_w = c.take(sizeof(float) * (size_t)p.rows);
   p.o_slot_row = c.take(sizeof(int32_t) * (size_t)(p.R > 0 ? p.R : 1));
   p.o_H = c.take(esz * (size_t)p.rows * p.inter);
+  if (p.direct || keep_rows) {  // one row per token, or per-row outputs kept: no split
+    p.dn.grid /= p.dn.ksplit;
+    p.dn.ksplit = 1;
+  }
   p.o_Y = p.direct ? c.take(0) : c.take(sizeof(float) * (size_t)p.dn.ksplit * p.rows * p.d);
 }
 

@@ -6,40 +6,20 @@
 //           or, when every token owns exactly one row, y[tok(r)] = Y[r] directly
 // combine:  y_i = sum over the token's routes (slot order) of Y[row], + shared row
 //
-// bf16 path: MFMA (v_mfma_f32_32x32x16_bf16 / v_mfma_f32_16x16x32_bf16), LDS
-// double-buffered BK=64 tiles with an XOR swizzle of 16-byte chunks, device-
-// side tile lists (no host synchronisation on group sizes), XCD-aware tile
-// order.  Weights are [rows, K] with K contiguous, so both operands load along K.
+// Weights are [rows, K] with K contiguous, so both operands load along K.  Group
+// sizes are device data: each kernel walks a device-side tile list built by the
+// permutation (no host synchronisation), in an XCD-aware order that keeps the
+// tiles sharing one weight tile on one XCD's L2.
+//
+// expert_gemm_tile: 128x128 macro tile, 4 waves of 32x32x16 bf16 MFMA, BK=64 LDS
+// double buffer with an XOR swizzle of 16-byte chunks, two tiles of global loads
+// in flight through registers.  The down projection may split its reduction
+// (few rows per retained expert): split s writes its own partial Y[s], and the
+// combine adds the splits in a fixed order.
 #include "common.hpp"
 #include "kernels.hpp"
 
 namespace exfold {
-
-template <int MF> struct Mfma;
-template <> struct Mfma<32> {
-  typedef f32x16 acc_t;
-  static constexpr int kRegs = 16;
-  static constexpr int kSteps = 4;  // BK=64 / 16
-  __device__ static __forceinline__ acc_t mma(bf16x8 a, bf16x8 b, acc_t c) {
-    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
-  }
-  __device__ static __forceinline__ int frag_row(int lane) { return lane & 31; }
-  __device__ static __forceinline__ int frag_chunk(int ks, int lane) { return ks * 2 + (lane >> 5); }
-  __device__ static __forceinline__ int out_row(int lane, int r) { return (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3); }
-  __device__ static __forceinline__ int out_col(int lane) { return lane & 31; }
-};
-template <> struct Mfma<16> {
-  typedef f32x4 acc_t;
-  static constexpr int kRegs = 4;
-  static constexpr int kSteps = 2;  // BK=64 / 32
-  __device__ static __forceinline__ acc_t mma(bf16x8 a, bf16x8 b, acc_t c) {
-    return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-  }
-  __device__ static __forceinline__ int frag_row(int lane) { return lane & 15; }
-  __device__ static __forceinline__ int frag_chunk(int ks, int lane) { return ks * 4 + (lane >> 4); }
-  __device__ static __forceinline__ int out_row(int lane, int r) { return (lane >> 4) * 4 + r; }
-  __device__ static __forceinline__ int out_col(int lane) { return lane & 15; }
-};
 
 struct GemmKArgs {
   const bf16_t *A;  // gate_up: x [T, d] gathered by row_token; down: H [rows, I]
@@ -47,13 +27,12 @@ struct GemmKArgs {
   const int32_t *row_token;
   const int32_t *offsets;
   const int32_t *tile_start;
-  int groups, n_experts, n_tiles, ksplit, kc;
+  int groups, n_experts, n_tiles, ksplit, kc, rows;
   const bf16_t *W, *Ws;  // routed base and shared expert
   long long w_stride;    // elements per routed expert
   int ldw;               // K extent of a weight row
   int inter;             // gate_up: intermediate size (up-row offset, H width)
   int d;                 // down: output width
-  int rows;
   bf16_t *H;
   float *Y;
   bf16_t *y;
@@ -67,165 +46,202 @@ constexpr int kBK = 64;
 // LDS element offset of 16-byte chunk q of tile row r (8 chunks per 128-byte row).
 __device__ __forceinline__ int swz(int r, int q) { return (r * 8 + (q ^ (r & 7))) * 8; }
 
-template <int BM, int BN, int WM, int WN, int MF, bool GATE_UP, bool DIRECT>
-__global__ __launch_bounds__(256) void expert_gemm_bf16(const GemmKArgs p) {
-  typedef Mfma<MF> M;
-  constexpr int WTM = BM / WM, WTN = BN / WN;
-  constexpr int TM = WTM / MF, TN = WTN / MF;
-  constexpr int PA = BM * 8 / 256, PB = BN * 8 / 256;
-  static_assert(WM * WN == 4, "4 waves");
-  static_assert(TM >= 1 && TN >= 1 && PA >= 1 && PB >= 1, "tile shape");
-  static_assert(!GATE_UP || (TN % 2 == 0), "gate/up pairs");
-
-  __shared__ __attribute__((aligned(16))) bf16_t As[2][BM * kBK];
-  __shared__ __attribute__((aligned(16))) bf16_t Bs[2][BN * kBK];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-
-  // ---- tile decode: (group, n-tile, k-split) outer, m-tile inner ----
-  const int L = xcd_remap(blockIdx.x, gridDim.x);
+// Tile of workgroup `wg`: group g, n-tile nt, split ks, m-tile mt (m-tile
+// fastest, so the m-tiles sharing one weight tile run together).  The grid is an
+// upper bound of the tile count; workgroups past the device-side count exit, and
+// the XCD-aware remap is taken over the actual count so that every XCD gets an
+// equal, contiguous share of the real tiles.
+struct TileId {
+  int g, nt, ks, mt;
+};
+__device__ __forceinline__ bool decode_tile(const GemmKArgs &p, int wg, TileId &t) {
   const int units = p.n_tiles * p.ksplit;
   const int total = p.tile_start[p.groups] * units;
-  if (L >= total) return;
+  if (wg >= total) return false;
+  const int L = xcd_remap(wg, total);
   int lo = 0, hi = p.groups;
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
     if (p.tile_start[mid] * units <= L) lo = mid; else hi = mid;
   }
-  const int g = lo;
-  const int mt_g = p.tile_start[g + 1] - p.tile_start[g];
-  const int local = L - p.tile_start[g] * units;
-  const int mt = local % mt_g;
-  const int rest = local / mt_g;
-  const int ks = rest % p.ksplit;
-  const int nt = rest / p.ksplit;
-  const int row0 = p.offsets[g] + mt * BM;
-  const int valid = min(BM, p.offsets[g + 1] - row0);
-  const bf16_t *Wg = (g < p.n_experts) ? p.W + (long long)g * p.w_stride : p.Ws;
-  const int k_begin = ks * p.kc;
+  const int mt_g = p.tile_start[lo + 1] - p.tile_start[lo];
+  const int local = L - p.tile_start[lo] * units;
+  t.g = lo;
+  t.mt = local % mt_g;
+  const int u = local / mt_g;
+  t.ks = u % p.ksplit;
+  t.nt = u / p.ksplit;
+  return true;
+}
 
-  // ---- per-thread global source rows ----
+// ---------------------------------------------------------------------------
+// Macro-tile kernel.
+// ---------------------------------------------------------------------------
+template <int BM, int BN, int STAGES, bool GATE_UP, bool DIRECT>
+__global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
+  constexpr int WTM = BM / 2, WTN = BN / 2;
+  constexpr int TM = WTM / 32, TN = WTN / 32;
+  constexpr int PA = BM / 32, PB = BN / 32;  // 16-byte chunks per thread per stage
+  static_assert(!GATE_UP || (TN % 2 == 0), "gate/up pairs");
+
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * (BM + BN) * kBK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  TileId t;
+  if (!decode_tile(p, blockIdx.x, t)) return;
+  const int row0 = p.offsets[t.g] + t.mt * BM;
+  const int valid = min(BM, p.offsets[t.g + 1] - row0);
+  const bf16_t *Wg = (t.g < p.n_experts) ? p.W + (long long)t.g * p.w_stride : p.Ws;
+
+  // global source of this thread's 16-byte chunks (row r = c / 8, chunk q = c % 8)
   const bf16_t *a_src[PA];
   const bf16_t *b_src[PB];
 #pragma unroll
   for (int i = 0; i < PA; ++i) {
     const int c = i * 256 + tid;
-    const int r = c >> 3, q = c & 7;
+    const int r = c >> 3;
     const int rr = row0 + (r < valid ? r : 0);
     const long long arow = GATE_UP ? (long long)p.row_token[rr] : (long long)rr;
-    a_src[i] = p.A + arow * p.lda + k_begin + q * 8;
+    a_src[i] = p.A + arow * p.lda + t.ks * p.kc + (c & 7) * 8;
   }
 #pragma unroll
   for (int i = 0; i < PB; ++i) {
     const int c = i * 256 + tid;
-    const int r = c >> 3, q = c & 7;
+    const int r = c >> 3;
     int wrow;
     if (GATE_UP)
-      wrow = (r < BN / 2) ? nt * (BN / 2) + r : p.inter + nt * (BN / 2) + (r - BN / 2);
+      wrow = (r < BN / 2) ? t.nt * (BN / 2) + r : p.inter + t.nt * (BN / 2) + (r - BN / 2);
     else
-      wrow = nt * BN + r;
-    b_src[i] = Wg + (long long)wrow * p.ldw + k_begin + q * 8;
+      wrow = t.nt * BN + r;
+    b_src[i] = Wg + (long long)wrow * p.ldw + t.ks * p.kc + (c & 7) * 8;
   }
 
-  uint4 ra[PA], rb[PB];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < PA; ++i) ra[i] = *reinterpret_cast<const uint4 *>(a_src[i] + k0);
-#pragma unroll
-    for (int i = 0; i < PB; ++i) rb[i] = *reinterpret_cast<const uint4 *>(b_src[i] + k0);
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < PA; ++i) {
-      const int c = i * 256 + tid;
-      *reinterpret_cast<uint4 *>(&As[buf][swz(c >> 3, c & 7)]) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < PB; ++i) {
-      const int c = i * 256 + tid;
-      *reinterpret_cast<uint4 *>(&Bs[buf][swz(c >> 3, c & 7)]) = rb[i];
-    }
-  };
-
-  typename M::acc_t acc[TM][TN];
+  f32x16 acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
     for (int j = 0; j < TN; ++j)
 #pragma unroll
-      for (int r = 0; r < M::kRegs; ++r) acc[i][j][r] = 0.f;
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  // B-tile row of wave subtile j (gate/up pairs for GATE_UP)
-  auto b_row0 = [&](int j) {
-    if (GATE_UP)
-      return (j < TN / 2) ? wn * (WTN / 2) + j * MF : BN / 2 + wn * (WTN / 2) + (j - TN / 2) * MF;
-    return wn * WTN + j * MF;
-  };
+  // LDS row of wave subtile j of B (gate/up pairs for GATE_UP)
+  int b_row[TN];
+#pragma unroll
+  for (int j = 0; j < TN; ++j)
+    b_row[j] = GATE_UP ? ((j < TN / 2) ? wn * (WTN / 2) + j * 32 : BN / 2 + wn * (WTN / 2) + (j - TN / 2) * 32)
+                       : wn * WTN + j * 32;
 
+  // The prefetch registers are plain arrays indexed only by unrolled constants
+  // (macros, not lambdas taking their address), so they stay in VGPRs.
+#define EXF_GLOAD(RA, RB, K0)                                                                \
+  do {                                                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < PA; ++i_) RA[i_] =                               \
+        *reinterpret_cast<const u32x4 *>(a_src[i_] + (K0));                                  \
+    _Pragma("unroll") for (int i_ = 0; i_ < PB; ++i_) RB[i_] =                               \
+        *reinterpret_cast<const u32x4 *>(b_src[i_] + (K0));                                  \
+  } while (0)
+#define EXF_LSTORE(RA, RB, BUF)                                                              \
+  do {                                                                                       \
+    bf16_t *As_ = smem + (BUF) * BM * kBK;                                                   \
+    bf16_t *Bs_ = smem + 2 * BM * kBK + (BUF) * BN * kBK;                                    \
+    _Pragma("unroll") for (int i_ = 0; i_ < PA; ++i_) {                                      \
+      const int c_ = i_ * 256 + tid;                                                         \
+      *reinterpret_cast<u32x4 *>(&As_[swz(c_ >> 3, c_ & 7)]) = RA[i_];                        \
+    }                                                                                        \
+    _Pragma("unroll") for (int i_ = 0; i_ < PB; ++i_) {                                      \
+      const int c_ = i_ * 256 + tid;                                                         \
+      *reinterpret_cast<u32x4 *>(&Bs_[swz(c_ >> 3, c_ & 7)]) = RB[i_];                        \
+    }                                                                                        \
+  } while (0)
+#define EXF_COMPUTE(BUF)                                                                     \
+  do {                                                                                       \
+    const bf16_t *As_ = smem + (BUF) * BM * kBK;                                             \
+    const bf16_t *Bs_ = smem + 2 * BM * kBK + (BUF) * BN * kBK;                              \
+    _Pragma("unroll") for (int s_ = 0; s_ < 4; ++s_) {                                       \
+      bf16x8 a_[TM], b_[TN];                                                                 \
+      const int ch_ = s_ * 2 + (lane >> 5);                                                  \
+      _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_) a_[i_] =                             \
+          *reinterpret_cast<const bf16x8 *>(&As_[swz(wm * WTM + i_ * 32 + (lane & 31), ch_)]); \
+      _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) b_[j_] =                             \
+          *reinterpret_cast<const bf16x8 *>(&Bs_[swz(b_row[j_] + (lane & 31), ch_)]);         \
+      _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_)                                      \
+          _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) acc[i_][j_] =                    \
+              __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_[i_], b_[j_], acc[i_][j_], 0, 0, 0); \
+    }                                                                                        \
+  } while (0)
+
+  // Pairs of phases over the two LDS buffers, no early exit (one loop exit keeps
+  // the accumulators in one register set); an odd tile count ends with buffer 0.
   const int KT = p.kc / kBK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) gload((kt + 1) * kBK);
-#pragma unroll
-    for (int s = 0; s < M::kSteps; ++s) {
-      bf16x8 a[TM], b[TN];
-      const int ch = M::frag_chunk(s, lane);
-#pragma unroll
-      for (int i = 0; i < TM; ++i) {
-        const int m = wm * WTM + i * MF + M::frag_row(lane);
-        a[i] = *reinterpret_cast<const bf16x8 *>(&As[cur][swz(m, ch)]);
-      }
-#pragma unroll
-      for (int j = 0; j < TN; ++j) {
-        const int n = b_row0(j) + M::frag_row(lane);
-        b[j] = *reinterpret_cast<const bf16x8 *>(&Bs[cur][swz(n, ch)]);
-      }
-#pragma unroll
-      for (int i = 0; i < TM; ++i)
-#pragma unroll
-        for (int j = 0; j < TN; ++j) acc[i][j] = M::mma(a[i], b[j], acc[i][j]);
-    }
-    if (kt + 1 < KT) lstore(cur ^ 1);
+  if (STAGES == 2) {
+    // LDS buffer (kt & 1) holds tile kt; the other register set holds tile kt + 1,
+    // so each tile's loads are covered by two compute phases.
+    u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
+    EXF_GLOAD(ra0, rb0, 0);
+    EXF_LSTORE(ra0, rb0, 0);
+    if (KT > 1) EXF_GLOAD(ra1, rb1, kBK);
     __syncthreads();
+    int kt = 0;
+    for (; kt + 2 <= KT; kt += 2) {
+      if (kt + 2 < KT) EXF_GLOAD(ra0, rb0, (kt + 2) * kBK);
+      EXF_COMPUTE(0);
+      EXF_LSTORE(ra1, rb1, 1);
+      __syncthreads();
+      if (kt + 3 < KT) EXF_GLOAD(ra1, rb1, (kt + 3) * kBK);
+      EXF_COMPUTE(1);
+      if (kt + 2 < KT) EXF_LSTORE(ra0, rb0, 0);
+      __syncthreads();
+    }
+    if (kt < KT) EXF_COMPUTE(0);
+  } else {
+    // One tile of loads in flight, covered by one compute phase.
+    u32x4 ra[PA], rb[PB];
+    EXF_GLOAD(ra, rb, 0);
+    EXF_LSTORE(ra, rb, 0);
+    __syncthreads();
+    int kt = 0;
+    for (; kt + 2 <= KT; kt += 2) {
+      EXF_GLOAD(ra, rb, (kt + 1) * kBK);
+      EXF_COMPUTE(0);
+      EXF_LSTORE(ra, rb, 1);
+      __syncthreads();
+      if (kt + 2 < KT) EXF_GLOAD(ra, rb, (kt + 2) * kBK);
+      EXF_COMPUTE(1);
+      if (kt + 2 < KT) EXF_LSTORE(ra, rb, 0);
+      __syncthreads();
+    }
+    if (kt < KT) EXF_COMPUTE(0);
   }
+#undef EXF_GLOAD
+#undef EXF_LSTORE
+#undef EXF_COMPUTE
 
   // ---- epilogue ----
-  if (GATE_UP) {
 #pragma unroll
-    for (int i = 0; i < TM; ++i)
+  for (int i = 0; i < TM; ++i) {
 #pragma unroll
-      for (int j = 0; j < TN / 2; ++j)
+    for (int j = 0; j < (GATE_UP ? TN / 2 : TN); ++j) {
 #pragma unroll
-        for (int r = 0; r < M::kRegs; ++r) {
-          const int ml = wm * WTM + i * MF + M::out_row(lane, r);
-          if (ml < valid) {
-            const int n = nt * (BN / 2) + wn * (WTN / 2) + j * MF + M::out_col(lane);
-            const float hv = silu(acc[i][j][r]) * acc[i][j + TN / 2][r];
-            p.H[(long long)(row0 + ml) * p.inter + n] = f32_to_bf16(hv);
-          }
-        }
-  } else {
-#pragma unroll
-    for (int i = 0; i < TM; ++i)
-#pragma unroll
-      for (int j = 0; j < TN; ++j)
-#pragma unroll
-        for (int r = 0; r < M::kRegs; ++r) {
-          const int ml = wm * WTM + i * MF + M::out_row(lane, r);
-          if (ml < valid) {
-            const int row = row0 + ml;
-            const int n = nt * BN + wn * WTN + j * MF + M::out_col(lane);
+      for (int r = 0; r < 16; ++r) {
+        const int ml = wm * WTM + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+        if (ml < valid) {
+          const int row = row0 + ml;
+          if (GATE_UP) {
+            const int n = t.nt * (BN / 2) + wn * (WTN / 2) + j * 32 + (lane & 31);
+            p.H[(long long)row * p.inter + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + TN / 2][r]);
+          } else {
+            const int n = t.nt * BN + wn * WTN + j * 32 + (lane & 31);
             const float v = acc[i][j][r] * p.row_w[row];
             if (DIRECT)
               p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v);
             else
-              p.Y[((long long)ks * p.rows + row) * p.d + n] = v;
+              p.Y[((long long)t.ks * p.rows + row) * p.d + n] = v;
           }
         }
+      }
+    }
   }
 }
 
@@ -303,44 +319,39 @@ static int largest_divisor_at_most(int n, int cap) {
 void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d, int inter,
                        int cu_count, GemmPlan *gu, GemmPlan *dn) {
   if (dtype != EXFOLD_BF16) {
-    *gu = GemmPlan{4, 64, 1, 0};
-    *dn = GemmPlan{4, 64, 1, 0};
+    *gu = GemmPlan{4, 64, 1, 0, kGemmSimt};
+    *dn = GemmPlan{4, 64, 1, 0, kGemmSimt};
     return;
   }
-  // Tile height from the rows each active group is expected to hold (not from
-  // the phase), so equal problems get equal plans whatever the phase.
+  // 128x128 tiles everywhere; the plan depends on the problem only (rows, groups,
+  // sizes), never on the phase, so equal problems get equal plans.
+  *gu = GemmPlan{128, 128, 1, 0, kGemmTile};
+  *dn = GemmPlan{128, 128, 1, 0, kGemmTile};
+  const int mt_max = rows / 128 + groups;  // >= sum over groups of ceil(rows_g / 128)
+  gu->grid = mt_max * (inter / 64);
+  // Few expected tiles (few rows per retained expert): split the down projection's
+  // reduction so the workgroups still cover every CU.  Partial sums land in
+  // separate buffers and are added in a fixed order by the combine.
   const int active = active_groups < 1 ? 1 : active_groups;
-  const bool small = rows <= 48 * active;
-  if (small) {
-    *gu = GemmPlan{32, 128, 1, 0};
-    *dn = GemmPlan{32, 128, 1, 0};
-  } else {
-    *gu = GemmPlan{128, 128, 1, 0};
-    *dn = GemmPlan{128, 128, 1, 0};
+  const int mt_expect = (rows + 127) / 128 > active ? (rows + 127) / 128 : active;
+  const int dn_tiles = mt_expect * (d / 128);
+  if (dn_tiles < 2 * cu_count) {
+    const int want = (2 * cu_count + dn_tiles - 1) / dn_tiles;
+    dn->ksplit = largest_divisor_at_most(inter / kBK, want > 8 ? 8 : want);
   }
-  const int mt_gu = rows / gu->bm + groups;
-  const int mt_dn = rows / dn->bm + groups;
-  gu->grid = mt_gu * (inter / (gu->bn / 2));
-  const int nt_dn = d / dn->bn;
-  if (small) {
-    // Split the down projection's reduction so that the few retained groups
-    // still spread over every CU.
-    const int want = (2 * cu_count + active * nt_dn - 1) / (active * nt_dn);
-    dn->ksplit = largest_divisor_at_most(inter / kBK, want < 1 ? 1 : want);
-  }
-  dn->grid = mt_dn * nt_dn * dn->ksplit;
+  dn->grid = mt_max * (d / 128) * dn->ksplit;
 }
 
-template <int BM, int BN, int WM, int WN, int MF>
-static void launch_pair(const GemmKArgs &gu_args, const GemmKArgs &dn_args, int gu_grid, int dn_grid,
+template <int BM, int BN, int STAGES>
+static void launch_tile(const GemmKArgs &ga, const GemmKArgs &da, int gu_grid, int dn_grid,
                         bool direct, hipStream_t s, hipEvent_t ev_mid) {
-  if (gu_grid > 0) expert_gemm_bf16<BM, BN, WM, WN, MF, true, false><<<gu_grid, 256, 0, s>>>(gu_args);
+  if (gu_grid > 0) expert_gemm_tile<BM, BN, STAGES, true, false><<<gu_grid, 256, 0, s>>>(ga);
   if (ev_mid) (void)hipEventRecord(ev_mid, s);
   if (dn_grid > 0) {
     if (direct)
-      expert_gemm_bf16<BM, BN, WM, WN, MF, false, true><<<dn_grid, 256, 0, s>>>(dn_args);
+      expert_gemm_tile<BM, BN, STAGES, false, true><<<dn_grid, 256, 0, s>>>(da);
     else
-      expert_gemm_bf16<BM, BN, WM, WN, MF, false, false><<<dn_grid, 256, 0, s>>>(dn_args);
+      expert_gemm_tile<BM, BN, STAGES, false, false><<<dn_grid, 256, 0, s>>>(da);
   }
 }
 
@@ -372,13 +383,13 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
   ga.n_tiles = a.inter / (gu.bn / 2);
   ga.ksplit = 1;
   ga.kc = a.d;
+  ga.rows = a.rows;
   ga.W = static_cast<const bf16_t *>(a.w_gate_up);
   ga.Ws = static_cast<const bf16_t *>(a.ws_gate_up);
   ga.w_stride = 2LL * a.inter * a.d;
   ga.ldw = a.d;
   ga.inter = a.inter;
   ga.d = a.d;
-  ga.rows = a.rows;
   ga.H = static_cast<bf16_t *>(a.H);
 
   GemmKArgs da{};
@@ -392,27 +403,24 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
   da.n_tiles = a.d / dn.bn;
   da.ksplit = dn.ksplit;
   da.kc = a.inter / dn.ksplit;
+  da.rows = a.rows;
   da.W = static_cast<const bf16_t *>(a.w_down);
   da.Ws = static_cast<const bf16_t *>(a.ws_down);
   da.w_stride = (long long)a.d * a.inter;
   da.ldw = a.inter;
   da.inter = a.inter;
   da.d = a.d;
-  da.rows = a.rows;
   da.Y = a.Y;
   da.y = static_cast<bf16_t *>(a.y);
   da.row_w = a.row_w;
 
-  if (gu.bm == 32)
-    launch_pair<32, 128, 1, 4, 16>(ga, da, gu.grid, dn.grid, a.direct, s, ev_mid);
-  else
-    launch_pair<128, 128, 2, 2, 32>(ga, da, gu.grid, dn.grid, a.direct, s, ev_mid);
+  launch_tile<128, 128, 2>(ga, da, gu.grid, dn.grid, a.direct, s, ev_mid);
   return hipGetLastError();
 }
 
 // ---------------------------------------------------------------------------
-// Weighted combine: y_i = sum_k sum_split Y[split][row(i,k)] (+ shared row),
-// in slot order; float32 accumulation, one rounding to the output dtype.
+// Weighted combine: y_i = sum_k Y[row(i,k)] (+ shared row), in slot order;
+// float32 accumulation, one rounding to the output dtype.
 // ---------------------------------------------------------------------------
 template <typename OutT>
 __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ Y, int ksplit,
@@ -420,18 +428,19 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
                                                      int k_out, int d, int shared_base,
                                                      OutT *__restrict__ y) {
   const int i = blockIdx.x;
+  const long long split = (long long)rows * d;
   for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int k = 0; k < k_out; ++k) {
-      const int r = slot_row[(long long)i * k_out + k];
+    for (int k = 0; k <= k_out; ++k) {
+      long long r;
+      if (k < k_out)
+        r = slot_row[(long long)i * k_out + k];
+      else if (shared_base >= 0)
+        r = shared_base + i;
+      else
+        break;
       for (int sp = 0; sp < ksplit; ++sp) {
-        const float4 v = *reinterpret_cast<const float4 *>(Y + ((long long)sp * rows + r) * d + c);
-        acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-      }
-    }
-    if (shared_base >= 0) {
-      for (int sp = 0; sp < ksplit; ++sp) {
-        const float4 v = *reinterpret_cast<const float4 *>(Y + ((long long)sp * rows + shared_base + i) * d + c);
+        const float4 v = *reinterpret_cast<const float4 *>(Y + sp * split + r * d + c);
         acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
       }
     }

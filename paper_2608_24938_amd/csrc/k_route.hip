@@ -15,51 +15,91 @@
 namespace exfold {
 
 // ---------------------------------------------------------------------------
-// Router logits.  bf16: one wave per 16 tokens, 16x16x32 bf16 MFMA over all
-// N experts (x read once, W_r stays in L2).  f32: one thread per logit.
+// Router logits.  bf16: a workgroup of KS waves takes 16 tokens; wave w reduces
+// its slice of d with 16x16x32 bf16 MFMA against all NT*16 (padded) experts, and
+// the KS partial sums are added in a fixed order through LDS.  W_r stays in L2.
+// f32: one thread per logit.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void router_logits_bf16(const bf16_t *__restrict__ x,
-                                                          const bf16_t *__restrict__ wr,
-                                                          const float *__restrict__ bias, int T,
-                                                          int N, int d, float *__restrict__ logits) {
+template <int NT, int KS>
+__global__ __launch_bounds__(64 * KS) void router_logits_bf16(const bf16_t *__restrict__ x,
+                                                              const bf16_t *__restrict__ wr,
+                                                              const float *__restrict__ bias,
+                                                              int T, int N, int d,
+                                                              float *__restrict__ logits) {
+  __shared__ float red[KS][NT * 4][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int t0 = (blockIdx.x * 4 + wave) * 16;
-  if (t0 >= T) return;
+  const int t0 = blockIdx.x * 16;
   const int row = min(t0 + (lane & 15), T - 1);
   const int kq = (lane >> 4) * 8;
-  const int n_tiles = (N + 15) >> 4;
-  f32x4 acc[16];
+  f32x4 acc[NT];
 #pragma unroll
-  for (int j = 0; j < 16; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int j = 0; j < NT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bf16_t *wrow[NT];
+  bool live[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int e = j * 16 + (lane & 15);
+    live[j] = e < N;
+    wrow[j] = wr + (size_t)(live[j] ? e : 0) * d + kq;
+  }
   const bf16_t *xa = x + (size_t)row * d + kq;
-  for (int k = 0; k < d; k += 32) {
-    const bf16x8 a = *reinterpret_cast<const bf16x8 *>(xa + k);
+  const int steps = d / 32;
+  const int s0 = wave * steps / KS, s1 = (wave + 1) * steps / KS;
+  bf16x8 zero;
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      if (j < n_tiles) {
-        const int e = j * 16 + (lane & 15);
-        bf16x8 b;
-        if (e < N) {
-          b = *reinterpret_cast<const bf16x8 *>(wr + (size_t)e * d + k + kq);
-        } else {
+  for (int q = 0; q < 8; ++q) zero[q] = (__bf16)0.0f;
+  int st = s0;
+  for (; st + 2 <= s1; st += 2) {
+    const int k = st * 32;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(xa + k);
+    const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(xa + k + 32);
+    bf16x8 b0[NT], b1[NT];
 #pragma unroll
-          for (int q = 0; q < 8; ++q) b[q] = (__bf16)0.0f;
-        }
-        acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[j], 0, 0, 0);
-      }
+    for (int j = 0; j < NT; ++j) {
+      b0[j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
+      b1[j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k + 32);
+    }
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, live[j] ? b0[j] : zero, acc[j], 0, 0, 0);
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, live[j] ? b1[j] : zero, acc[j], 0, 0, 0);
+    }
+  }
+  if (st < s1) {
+    const int k = st * 32;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(xa + k);
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, live[j] ? b0 : zero, acc[j], 0, 0, 0);
     }
   }
 #pragma unroll
-  for (int j = 0; j < 16; ++j) {
-    if (j < n_tiles) {
-      const int e = j * 16 + (lane & 15);
+  for (int j = 0; j < NT; ++j)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int t = t0 + (lane >> 4) * 4 + i;
-        if (t < T && e < N) logits[(size_t)t * N + e] = acc[j][i] + (bias ? bias[e] : 0.0f);
-      }
-    }
+    for (int i = 0; i < 4; ++i) red[wave][j * 4 + i][lane] = acc[j][i];
+  __syncthreads();
+  // entry (j, i, l): expert j*16 + l%16, token t0 + (l/16)*4 + i
+  for (int idx = threadIdx.x; idx < NT * 4 * 64; idx += 64 * KS) {
+    const int ji = idx >> 6, l = idx & 63;
+    const int j = ji >> 2, i = ji & 3;
+    float v = red[0][ji][l];
+#pragma unroll
+    for (int w = 1; w < KS; ++w) v += red[w][ji][l];
+    const int t = t0 + (l >> 4) * 4 + i;
+    const int e = j * 16 + (l & 15);
+    if (t < T && e < N) logits[(size_t)t * N + e] = v + (bias ? bias[e] : 0.0f);
   }
+}
+
+template <int NT>
+static void launch_router_nt(const bf16_t *x, const bf16_t *wr, const float *bias, int T, int N, int d,
+                             float *logits, hipStream_t s) {
+  const int blocks = (T + 15) / 16;
+  if (blocks < 512)
+    router_logits_bf16<NT, 8><<<blocks, 512, 0, s>>>(x, wr, bias, T, N, d, logits);
+  else
+    router_logits_bf16<NT, 4><<<blocks, 256, 0, s>>>(x, wr, bias, T, N, d, logits);
 }
 
 __global__ __launch_bounds__(256) void router_logits_f32(const float *__restrict__ x,
@@ -80,9 +120,14 @@ hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, 
                                 int T, int N, int d, float *logits, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   if (dtype == EXFOLD_BF16) {
-    const int waves = (T + 15) / 16;
-    router_logits_bf16<<<(waves + 3) / 4, 256, 0, s>>>(
-        static_cast<const bf16_t *>(x), static_cast<const bf16_t *>(w_router), bias, T, N, d, logits);
+    const bf16_t *xb = static_cast<const bf16_t *>(x);
+    const bf16_t *wb = static_cast<const bf16_t *>(w_router);
+    const int nt = (N + 15) / 16;
+    if (nt <= 1) launch_router_nt<1>(xb, wb, bias, T, N, d, logits, s);
+    else if (nt <= 2) launch_router_nt<2>(xb, wb, bias, T, N, d, logits, s);
+    else if (nt <= 4) launch_router_nt<4>(xb, wb, bias, T, N, d, logits, s);
+    else if (nt <= 8) launch_router_nt<8>(xb, wb, bias, T, N, d, logits, s);
+    else launch_router_nt<16>(xb, wb, bias, T, N, d, logits, s);
   } else {
     router_logits_f32<<<(T * N + 255) / 256, 256, 0, s>>>(
         static_cast<const float *>(x), static_cast<const float *>(w_router), bias, T, N, d, logits);

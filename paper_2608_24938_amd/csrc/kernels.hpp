@@ -40,9 +40,12 @@ hipError_t launch_permute(const int32_t *route_ids, const float *route_w, int T,
                           int t_shared, int bm0, int bm1, const PermBuffers &pb, hipStream_t s);
 
 // ---- expert GEMMs and combine (k_gemm.hip) ----
+enum { kGemmSimt = 0, kGemmTile = 1 };
 struct GemmPlan {
-  int bm, bn, ksplit;
-  int grid;
+  int bm, bn;  // tile height (rows) and width (output columns, or weight rows for gate/up)
+  int ksplit;  // splits of the reduction (down projection only; partial outputs)
+  int grid;    // workgroups launched (an upper bound on the device-side tile count)
+  int kind;    // kGemmSimt (float32 layers) or kGemmTile (bf16 MFMA tiles)
 };
 struct ExpertArgs {
   int dtype;
@@ -55,7 +58,7 @@ struct ExpertArgs {
   const float *row_w;
   int rows;     // R + T_shared
   void *H;      // [rows, I]
-  float *Y;     // [ksplit, rows, d] partial outputs (nullptr when direct)
+  float *Y;     // [ksplit, rows, d] per-row outputs (nullptr when direct)
   void *y;      // [T, d] direct output (each token owns exactly one row)
   bool direct;
 };

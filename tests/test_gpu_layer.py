@@ -216,3 +216,33 @@ def test_zero_tokens_is_a_noop():
     y = X.moe_forward(lp.dev, x, "prefill", 1, S, L, h)
     sync()
     assert y.shape == (0, 256)
+
+
+# Rows per active group select the expert kernel: <= 8, <= 24, <= 64 rows stream
+# the weights (16/32/64-row chunks); <= 384 use 128x128 LDS tiles; more use the
+# 256x256 direct-to-LDS tiles.  Group sizes are skewed so every path also sees
+# ragged groups, empty groups and partial tiles.
+PATH_SHAPES = {
+    "bf16-256x512": synth.LayerShape("paths", d=256, inter=512, n_experts=8, top_k=2, dtype="bf16"),
+    "bf16-384x192": synth.LayerShape("paths-odd", d=384, inter=192, n_experts=8, top_k=2, dtype="bf16"),
+}
+
+
+@pytest.mark.parametrize("shape_name", sorted(PATH_SHAPES))
+@pytest.mark.parametrize("T,k_out", [(48, 1), (150, 1), (400, 1), (1900, 1), (4096, 1), (2100, 2)])
+def test_execute_every_kernel_path(shape_name, T, k_out):
+    shape = PATH_SHAPES[shape_name]
+    lp = LayerPair(shape, seed=11)
+    rng = np.random.default_rng(T + k_out)
+    p = np.array([0.3, 0.2, 0.15, 0.12, 0.1, 0.08, 0.05, 0.0])   # expert 7 stays empty
+    ids = rng.choice(shape.n_experts, size=(T, k_out), p=p).astype(np.int32)
+    w = rng.standard_normal((T, k_out)).astype(np.float32)
+    xs = synth.tokens(shape, T, seed=11)
+    dbg = {"offsets": torch.empty(shape.n_experts + 2, dtype=torch.int32, device=DEV)}
+    y = X.moe_execute(lp.dev, to_dev(xs), to_dev(ids), to_dev(w), debug=dbg)
+    sync()
+    counts = np.diff(dbg["offsets"].cpu().numpy()[: shape.n_experts + 1])
+    np.testing.assert_array_equal(counts, np.bincount(ids.reshape(-1), minlength=shape.n_experts))
+    ref = O.moe_output(lp.ref, synth.widen(xs), ids, w)
+    err = per_token_rel_l2(from_dev(y), ref)
+    assert err.max() <= TOL_Y["bf16"], err.max()
