@@ -44,7 +44,9 @@ __device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g));
 constexpr int kBK = 64;
 
 // LDS element offset of 16-byte chunk q of tile row r (8 chunks per 128-byte row).
-__device__ __forceinline__ int swz(int r, int q) { return (r * 8 + (q ^ (r & 7))) * 8; }
+// The slot is q XOR gray(r): one chunk column of any 8 or 16 consecutive rows
+// (the lanes of one LDS cycle of ds_read_b128) then spans distinct banks.
+__device__ __forceinline__ int swz(int r, int q) { return (r * 8 + (q ^ ((r ^ (r >> 1)) & 7))) * 8; }
 
 // Tile of workgroup `wg`: group g, n-tile nt, split ks, m-tile mt (m-tile
 // fastest, so the m-tiles sharing one weight tile run together).  The grid is an
@@ -155,43 +157,77 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
       *reinterpret_cast<u32x4 *>(&Bs_[swz(c_ >> 3, c_ & 7)]) = RB[i_];                        \
     }                                                                                        \
   } while (0)
+// Fragments of k-step s+1 are read while the MFMAs of step s run.
+#define EXF_FRAGS(A_, B_, S_)                                                                \
+  do {                                                                                       \
+    const int ch_ = (S_) * 2 + (lane >> 5);                                                  \
+    _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_) A_[i_] =                               \
+        *reinterpret_cast<const bf16x8 *>(&As_[swz(wm * WTM + i_ * 32 + (lane & 31), ch_)]); \
+    _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) B_[j_] =                               \
+        *reinterpret_cast<const bf16x8 *>(&Bs_[swz(b_row[j_] + (lane & 31), ch_)]);           \
+  } while (0)
+#define EXF_MMA(A_, B_)                                                                      \
+  do {                                                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_)                                        \
+        _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) acc[i_][j_] =                      \
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(A_[i_], B_[j_], acc[i_][j_], 0, 0, 0);   \
+  } while (0)
 #define EXF_COMPUTE(BUF)                                                                     \
   do {                                                                                       \
     const bf16_t *As_ = smem + (BUF) * BM * kBK;                                             \
     const bf16_t *Bs_ = smem + 2 * BM * kBK + (BUF) * BN * kBK;                              \
-    _Pragma("unroll") for (int s_ = 0; s_ < 4; ++s_) {                                       \
-      bf16x8 a_[TM], b_[TN];                                                                 \
-      const int ch_ = s_ * 2 + (lane >> 5);                                                  \
-      _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_) a_[i_] =                             \
-          *reinterpret_cast<const bf16x8 *>(&As_[swz(wm * WTM + i_ * 32 + (lane & 31), ch_)]); \
-      _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) b_[j_] =                             \
-          *reinterpret_cast<const bf16x8 *>(&Bs_[swz(b_row[j_] + (lane & 31), ch_)]);         \
-      _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_)                                      \
-          _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) acc[i_][j_] =                    \
-              __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_[i_], b_[j_], acc[i_][j_], 0, 0, 0); \
-    }                                                                                        \
+    bf16x8 a0_[TM], b0_[TN], a1_[TM], b1_[TN];                                               \
+    EXF_FRAGS(a0_, b0_, 0);                                                                  \
+    EXF_FRAGS(a1_, b1_, 1);                                                                  \
+    EXF_MMA(a0_, b0_);                                                                       \
+    EXF_FRAGS(a0_, b0_, 2);                                                                  \
+    EXF_MMA(a1_, b1_);                                                                       \
+    EXF_FRAGS(a1_, b1_, 3);                                                                  \
+    EXF_MMA(a0_, b0_);                                                                       \
+    EXF_MMA(a1_, b1_);                                                                       \
+  } while (0)
+
+  // Schedule of one phase: the next tile's global loads first, fragments of
+  // k-step s+1 read while the MFMAs of step s run, and the staged tile written to
+  // the other LDS buffer before the last MFMA group.
+#define EXF_SCHEDULE()                                                               \
+  do {                                                                               \
+    __builtin_amdgcn_sched_group_barrier(0x020, PA + PB, 0); /* VMEM read */         \
+    __builtin_amdgcn_sched_group_barrier(0x100, 2 * (TM + TN), 0); /* DS read */     \
+    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN, 0); /* MFMA */              \
+    __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);                          \
+    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN, 0);                          \
+    __builtin_amdgcn_sched_group_barrier(0x100, TM + TN, 0);                          \
+    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN, 0);                          \
+    __builtin_amdgcn_sched_group_barrier(0x200, PA + PB, 0); /* DS write */           \
+    __builtin_amdgcn_sched_group_barrier(0x008, TM * TN, 0);                          \
   } while (0)
 
   // Pairs of phases over the two LDS buffers, no early exit (one loop exit keeps
   // the accumulators in one register set); an odd tile count ends with buffer 0.
+  // Loads past the last tile re-read the last tile (k clamped) and land in a
+  // buffer that is never read again, so each phase is one straight-line block.
   const int KT = p.kc / kBK;
+  const int k_last = (KT - 1) * kBK;
   if (STAGES == 2) {
     // LDS buffer (kt & 1) holds tile kt; the other register set holds tile kt + 1,
     // so each tile's loads are covered by two compute phases.
     u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
     EXF_GLOAD(ra0, rb0, 0);
     EXF_LSTORE(ra0, rb0, 0);
-    if (KT > 1) EXF_GLOAD(ra1, rb1, kBK);
+    EXF_GLOAD(ra1, rb1, min(kBK, k_last));
     __syncthreads();
     int kt = 0;
     for (; kt + 2 <= KT; kt += 2) {
-      if (kt + 2 < KT) EXF_GLOAD(ra0, rb0, (kt + 2) * kBK);
+      EXF_GLOAD(ra0, rb0, min((kt + 2) * kBK, k_last));
       EXF_COMPUTE(0);
       EXF_LSTORE(ra1, rb1, 1);
+      EXF_SCHEDULE();
       __syncthreads();
-      if (kt + 3 < KT) EXF_GLOAD(ra1, rb1, (kt + 3) * kBK);
+      EXF_GLOAD(ra1, rb1, min((kt + 3) * kBK, k_last));
       EXF_COMPUTE(1);
-      if (kt + 2 < KT) EXF_LSTORE(ra0, rb0, 0);
+      EXF_LSTORE(ra0, rb0, 0);
+      EXF_SCHEDULE();
       __syncthreads();
     }
     if (kt < KT) EXF_COMPUTE(0);
@@ -206,10 +242,12 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
       EXF_GLOAD(ra, rb, (kt + 1) * kBK);
       EXF_COMPUTE(0);
       EXF_LSTORE(ra, rb, 1);
+      EXF_SCHEDULE();
       __syncthreads();
-      if (kt + 2 < KT) EXF_GLOAD(ra, rb, (kt + 2) * kBK);
+      EXF_GLOAD(ra, rb, min((kt + 2) * kBK, k_last));
       EXF_COMPUTE(1);
-      if (kt + 2 < KT) EXF_LSTORE(ra, rb, 0);
+      EXF_LSTORE(ra, rb, 0);
+      EXF_SCHEDULE();
       __syncthreads();
     }
     if (kt < KT) EXF_COMPUTE(0);
@@ -217,6 +255,9 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
 #undef EXF_GLOAD
 #undef EXF_LSTORE
 #undef EXF_COMPUTE
+#undef EXF_FRAGS
+#undef EXF_MMA
+#undef EXF_SCHEDULE
 
   // ---- epilogue ----
 #pragma unroll
