@@ -15,14 +15,26 @@ roofline of the dominant kernel (the prefill gate/up GEMM, timed live with
 HIP events on its stream) and the CPU oracle timed on a bounded sample.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload mixtral|qwen3|glm|qwen3-decode]
+
+Two helper modes serve the committed profile summaries:
+
+    python bench.py --copy-calibration          # one 1 GiB device copy (counter scale)
+    python bench.py --prof-summary DIR          # markdown summary of the rocprofv3 runs in DIR
+
+`roofline.traffic` is read from the committed traffic summary of the dominant
+kernel, and only when the kernel sources still hash to what was profiled
+(otherwise it is null).
 """
 
 from __future__ import annotations
 
 import argparse
+import csv
 import ctypes
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -32,6 +44,11 @@ sys.path.insert(0, ROOT)
 METRIC = "folded MoE layer: prefill TFLOP/s + %MFMA peak; decode µs/layer + HBM GB/s"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+COPY_BYTES = 1 << 30        # size of the calibration copy
+DOMINANT = "expert_gemm_tile<128, 128, 2, true, false>"   # gate/up GEMM with fused SiLU*up
+KERNEL_SOURCES = ["paper_2608_24938_amd/csrc/k_gemm.hip", "paper_2608_24938_amd/csrc/common.hpp",
+                  "paper_2608_24938_amd/csrc/kernels.hpp", "paper_2608_24938_amd/build.py"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "expert_gemm_gate_up_mixtral_prefill_traffic.md")
 
 
 def log(*a):
@@ -72,6 +89,31 @@ class HipEvents:
         for ev in self.owned:
             self.hip.hipEventDestroy(ev)
         self.owned = []
+
+
+def kernel_sources_sha256():
+    """Hash of the sources that define the dominant kernel and its compile flags."""
+    h = hashlib.sha256()
+    for rel in KERNEL_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(workload):
+    """Scaled HBM bytes per launch of the dominant kernel from the committed summary, or None when the
+    summary is absent, covers another workload or was taken from different kernel sources."""
+    try:
+        text = open(TRAFFIC_FILE).read()
+    except OSError:
+        return None
+    m = re.search(r"^traffic-record: (\{.*\})\s*$", text, re.M)
+    if not m:
+        return None
+    rec = json.loads(m.group(1))
+    if rec.get("sources_sha256") != kernel_sources_sha256() or rec.get("workload") != workload:
+        return None
+    return rec
 
 
 def make_layer(shape, seed=0):
@@ -129,7 +171,18 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral", choices=["mixtral", "qwen3", "glm", "qwen3-decode"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run one plain 1 GiB device copy (the scale for the FETCH_SIZE/WRITE_SIZE counters)")
+    ap.add_argument("--prof-summary", metavar="DIR",
+                    help="print a markdown summary of the rocprofv3 runs under DIR (trace/, fetch/, write/, "
+                         "copyfetch/, copywrite/) and exit")
     args = ap.parse_args()
+    if args.prof_summary:
+        print(prof_summary(args.prof_summary, args.workload, args.steps))
+        return
+    if args.copy_calibration:
+        copy_calibration()
+        return
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the folded layer is measured "
               f"on a single MI355X and no multi-GPU path is built.", file=sys.stderr)
@@ -218,6 +271,14 @@ def main():
     log(f"prefill stages (us): {json.dumps({k: round(v, 1) for k, v in st_p.items()})}")
     log(f"decode stages (us): {json.dumps({k: round(v, 1) for k, v in st_d.items()})}")
 
+    # algorithmic bytes of one gate/up launch: the touched experts' gate/up weights, the gathered
+    # activations and the H it writes
+    esz = 2 if shape.dtype == "bf16" else 4
+    gu_rows = T * kp + (T if shape.shared_inter else 0)
+    n_groups = shape.n_experts + (1 if shape.shared_inter else 0)
+    gu_bytes = (2 * shape.inter * shape.d * n_groups + gu_rows * shape.d + gu_rows * shape.inter) * esz
+    traffic = recorded_traffic(args.workload)
+
     cpu = None
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(shape, host, xs_p, (S_np, L_np, h_np), kp)
@@ -243,8 +304,11 @@ def main():
                    "frac_hbm_peak": round(gbs_d / PEAK_HBM_GBS, 4), "experts_touched": touched,
                    "algorithmic_mb": round(bytes_d / 1e6, 2), "stages_us": {k: round(v, 1) for k, v in st_d.items()}},
         "roofline": {"bound": "mfma", "achieved": round(gu_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
-                     "kernel": "expert_gemm_bf16 gate/up (+SiLU*up), prefill",
+                     "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4),
+                     "traffic": None if traffic is None else traffic["bytes_per_launch"],
+                     "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
+                     "algorithmic_bytes": gu_bytes,
+                     "kernel": DOMINANT + " (prefill gate/up GEMM, fused SiLU*up)",
                      "per_launch_gflop": round(gu_flops / 1e9, 2), "avg_launch_us": round(st_p["gate_up"], 1)},
         "cpu_baseline": cpu,
     }
@@ -252,8 +316,10 @@ def main():
     print(json.dumps(rec), flush=True)
 
 
-def cpu_baseline(shape, host, xs_p, tables, kp, n_tokens=32):
-    """The oracle, as it stands, on the first n_tokens of the prefill batch (folded layer)."""
+def cpu_baseline(shape, host, xs_p, tables, kp, target_s=15.0, probe_tokens=64):
+    """The oracle, as it stands, on a bounded prefix of the prefill batch (folded layer).  The prefix
+    grows 4x per run (from probe_tokens) until a run takes target_s/2 or covers the whole batch; the
+    last run is the one reported."""
     import numpy as np
     from oracle import exfold_oracle as O
     from paper_2608_24938_amd import synth
@@ -267,16 +333,105 @@ def cpu_baseline(shape, host, xs_p, tables, kp, n_tokens=32):
                   w_down=lambda e: widen(host["dn"][e]), router_bias=host["bias"],
                   ws_gate_up=None if host["sgu"] is None else widen(host["sgu"]),
                   ws_down=None if host["sdn"] is None else widen(host["sdn"]))
-    x = widen(xs_p[:n_tokens])
     S, L, h = tables
-    t0 = time.perf_counter()
-    O.moe_forward(ref, x, shape.top_k, "prefill", kp, S, L, h)
-    dt = time.perf_counter() - t0
+
+    def timed(n):
+        x = widen(xs_p[:n])
+        t0 = time.perf_counter()
+        O.moe_forward(ref, x, shape.top_k, "prefill", kp, S, L, h)
+        return time.perf_counter() - t0
+
+    n_tokens = min(probe_tokens, xs_p.shape[0])
+    dt = timed(n_tokens)
+    while dt < target_s / 2 and n_tokens < xs_p.shape[0]:
+        log(f"cpu oracle: {n_tokens} tokens in {dt:.2f}s")
+        n_tokens = min(xs_p.shape[0], 4 * n_tokens)
+        dt = timed(n_tokens)
     flops = prefill_flops(shape, n_tokens, kp)
     log(f"cpu oracle: {n_tokens} tokens in {dt:.2f}s")
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"first {n_tokens} of the {xs_p.shape[0]} prefill tokens, folded layer (float64 NumPy), "
                       f"{dt:.2f} s wall", "seconds": round(dt, 3)}
+
+
+def copy_calibration():
+    """One plain device-to-device copy of COPY_BYTES (after a warm-up copy): the kernel whose FETCH_SIZE and
+    WRITE_SIZE counter values scale the counters of the other kernels to bytes."""
+    import torch
+    src = torch.ones(COPY_BYTES // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        torch.mul(src, 1.0, out=dst)   # an elementwise kernel: reads COPY_BYTES, writes COPY_BYTES
+    torch.cuda.synchronize()
+    log(f"copied {COPY_BYTES} bytes twice")
+
+
+def _counters(path):
+    out = {}
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            key = (r["Kernel_Name"], int(r["Grid_Size"]))
+            out.setdefault(key, {}).setdefault(r["Counter_Name"], []).append(float(r["Counter_Value"]))
+    return out
+
+
+def _find(dirname, suffix):
+    for root, _, files in os.walk(dirname):
+        for f in files:
+            if f.endswith(suffix):
+                return os.path.join(root, f)
+    raise FileNotFoundError(f"no *{suffix} under {dirname}")
+
+
+def prof_summary(d, workload, steps):
+    """Markdown summary of the rocprofv3 runs under d; `steps` is the --steps of the traced run, whose
+    last `steps` launches of each kernel are the timed ones."""
+    mean = lambda v: sum(v) / len(v)
+    cf = _counters(_find(os.path.join(d, "copyfetch"), "counter_collection.csv"))
+    cw = _counters(_find(os.path.join(d, "copywrite"), "counter_collection.csv"))
+    # the calibration copy is the launch that reads the most (the buffer fill before it only writes)
+    ck = max(cf, key=lambda k: mean(cf[k]["FETCH_SIZE"]))
+    fetch_kib = mean(cf[ck]["FETCH_SIZE"])
+    write_kib = mean(cw[ck]["WRITE_SIZE"])
+    f_fac = COPY_BYTES / (fetch_kib * 1024)
+    w_fac = COPY_BYTES / (write_kib * 1024)
+    lines = [f"copy calibration: kernel `{ck[0]}` copying {COPY_BYTES} B reads FETCH_SIZE {fetch_kib:.0f} KiB and "
+             f"WRITE_SIZE {write_kib:.0f} KiB per dispatch -> scale FETCH_SIZE x{f_fac:.4f}, WRITE_SIZE x{w_fac:.4f}",
+             ""]
+    trace = _find(os.path.join(d, "trace"), "kernel_trace.csv")
+    durs = {}
+    with open(trace) as f:
+        for r in csv.DictReader(f):
+            grid = int(r["Grid_Size_X"]) * int(r["Grid_Size_Y"]) * int(r["Grid_Size_Z"])
+            key = (r["Kernel_Name"], grid)
+            durs.setdefault(key, []).append((int(r["End_Timestamp"]) - int(r["Start_Timestamp"])) / 1e3)
+    fe = _counters(_find(os.path.join(d, "fetch"), "counter_collection.csv"))
+    wr = _counters(_find(os.path.join(d, "write"), "counter_collection.csv"))
+    lines.append("| kernel | grid (work-items) | launches | avg us | avg us, timed steps | min us | "
+                 "HBM read MB/launch | HBM write MB/launch |")
+    lines.append("|---|---|---|---|---|---|---|---|")
+    record = None
+    for key, v in sorted(durs.items(), key=lambda kv: -sum(kv[1])):
+        name = key[0].replace("exfold::", "").replace("(GemmKArgs)", "").replace("void ", "")
+        rd = mean(fe[key]["FETCH_SIZE"]) * 1024 * f_fac if key in fe else None
+        wt = mean(wr[key]["WRITE_SIZE"]) * 1024 * w_fac if key in wr else None
+        fmt = lambda b: "-" if b is None else f"{b / 1e6:.1f}"
+        timed = mean(v[-steps:]) if len(v) >= steps else mean(v)
+        lines.append(f"| `{name[:80]}` | {key[1]} | {len(v)} | {mean(v):.1f} | {timed:.1f} | {min(v):.1f} | "
+                     f"{fmt(rd)} | {fmt(wt)} |")
+        if record is None and DOMINANT in key[0] and rd is not None and wt is not None:
+            record = {"workload": workload, "kernel": DOMINANT, "grid": key[1], "avg_us": round(mean(v), 1),
+                      "avg_us_timed_steps": round(timed, 1),
+                      "fetch_bytes": round(rd), "write_bytes": round(wt), "bytes_per_launch": round(rd + wt),
+                      "fetch_scale": round(f_fac, 4), "write_scale": round(w_fac, 4),
+                      "sources_sha256": kernel_sources_sha256()}
+    lines.append("")
+    if record is not None:
+        lines.append("The dominant kernel is the launch of the prefill gate/up GEMM with the largest total time; "
+                     "its traffic (read + write, scaled) per launch:")
+        lines.append("")
+        lines.append("traffic-record: " + json.dumps(record))
+    return "\n".join(lines)
 
 
 if __name__ == "__main__":
