@@ -119,10 +119,7 @@ inline void record(void *const *events, int i, hipStream_t s) {
   if (events && events[i]) (void)hipEventRecord(static_cast<hipEvent_t>(events[i]), s);
 }
 
-exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
-                       const int32_t *route_ids, const float *route_w, void *y, void *ws,
-                       int32_t *offsets_dbg, int32_t *row_slot_dbg, bool keep_rows,
-                       hipStream_t s, void *const *events = nullptr) {
+PermBuffers perm_buffers(const ExecPlan &p, void *ws, int32_t *offsets_dbg, int32_t *row_slot_dbg) {
   PermBuffers pb;
   pb.blk_counts = at<int32_t>(ws, p.o_blk);
   pb.offsets = offsets_dbg ? offsets_dbg : at<int32_t>(ws, p.o_offsets);
@@ -132,8 +129,18 @@ exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
   pb.row_slot = row_slot_dbg ? row_slot_dbg : at<int32_t>(ws, p.o_row_slot);
   pb.row_w = at<float>(ws, p.o_row_w);
   pb.slot_row = at<int32_t>(ws, p.o_slot_row);
-  if (launch_permute(route_ids, route_w, p.T, p.k_out, p.N, p.t_shared, p.gu.bm, p.dn.bm, pb, s) !=
-      hipSuccess)
+  return pb;
+}
+
+// permuted: the routes were already permuted into pb (the decode front end).
+exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
+                       const int32_t *route_ids, const float *route_w, void *y, void *ws,
+                       int32_t *offsets_dbg, int32_t *row_slot_dbg, bool keep_rows,
+                       hipStream_t s, void *const *events = nullptr, bool permuted = false) {
+  const PermBuffers pb = perm_buffers(p, ws, offsets_dbg, row_slot_dbg);
+  if (!permuted &&
+      launch_permute(route_ids, route_w, p.T, p.k_out, p.N, p.t_shared, p.gu.bm, p.dn.bm, pb, s) !=
+          hipSuccess)
     return EXFOLD_ERR_DEVICE;
   record(events, EXFOLD_EV_PERMUTE, s);
   ExpertArgs a{};
@@ -171,7 +178,7 @@ exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
 }
 
 struct ForwardPlan {
-  int T = 0, N = 0, K = 0, k_out = 0, phase = 0, budget = 0, dcap = 0;
+  int T = 0, N = 0, K = 0, k_out = 0, phase = 0, budget = 0, dcap = 0, P = 1;
   size_t o_logits = 0, o_topk_ids = 0, o_topk_w = 0, o_keep = 0, o_pool = 0, o_pool_size = 0,
          o_tgt = 0, o_scl = 0, o_fold_ids = 0, o_fold_w = 0;
   ExecPlan ex;
@@ -194,8 +201,9 @@ exfold_status plan_forward(const exfold_layer *L, int64_t T, int32_t phase, int6
   p.budget = (int)(budget > (1 << 20) ? (1 << 20) : budget);
   p.k_out = (phase == EXFOLD_PHASE_PREFILL) ? (p.budget < p.K ? p.budget : p.K) : p.K;
   p.dcap = (p.budget < p.N) ? p.budget : p.N;
+  p.P = router_splits(L->dtype, p.T, p.N, (int)L->d);
   Carver c;
-  p.o_logits = c.take(sizeof(float) * (size_t)p.T * p.N);
+  p.o_logits = c.take(sizeof(float) * (size_t)p.P * p.T * p.N);  // router partial sums
   p.o_topk_ids = c.take(sizeof(int32_t) * (size_t)p.T * p.K);
   p.o_topk_w = c.take(sizeof(float) * (size_t)p.T * p.K);
   p.o_keep = c.take((size_t)p.T * p.K);
@@ -230,7 +238,7 @@ exfold_status plan_execute(const exfold_layer *L, int64_t T, int64_t k_out, Exec
 }
 
 struct CalibPlan {
-  int m = 0, N = 0, K = 0, kr = 0;
+  int m = 0, N = 0, K = 0, kr = 0, P = 1;
   size_t o_logits = 0, o_topk_ids = 0, o_topk_w = 0, o_route_ids = 0, o_route_w = 0, o_pos = 0,
          o_gram = 0;
   ExecPlan ex;
@@ -248,8 +256,9 @@ exfold_status plan_calibrate(const exfold_layer *L, int64_t m, int32_t mode, Cal
   p.K = (int)L->top_k;
   p.kr = (mode == EXFOLD_CAL_COMMON) ? p.N : p.K;
   if ((int64_t)p.m * p.kr > kMaxSlots) return EXFOLD_ERR_SHAPE;
+  p.P = router_splits(L->dtype, p.m, p.N, (int)L->d);
   Carver c;
-  p.o_logits = c.take(sizeof(float) * (size_t)p.m * p.N);
+  p.o_logits = c.take(sizeof(float) * (size_t)p.P * p.m * p.N);  // router partial sums
   p.o_topk_ids = c.take(sizeof(int32_t) * (size_t)p.m * p.K);
   p.o_topk_w = c.take(sizeof(float) * (size_t)p.m * p.K);
   p.o_route_ids = c.take(sizeof(int32_t) * (size_t)p.m * p.kr);
@@ -296,8 +305,9 @@ exfold_status exfold_select_prefill(const float *logits, int64_t T, int64_t N, i
   if (T == 0) return EXFOLD_OK;
   if (!h || !topk_ids || !topk_w || !keep) return EXFOLD_ERR_NULL;
   const int kp = (int)(k_pre > K ? K : k_pre);
-  if (launch_route_tokens(logits, (int)T, (int)N, (int)K, kp, h, nullptr, nullptr, topk_ids, topk_w,
-                          keep, nullptr, nullptr, nullptr, static_cast<hipStream_t>(stream)) != hipSuccess)
+  if (launch_route_tokens(logits, 1, nullptr, nullptr, (int)T, (int)N, (int)K, kp, h, nullptr, nullptr,
+                          topk_ids, topk_w, keep, nullptr, nullptr, nullptr,
+                          static_cast<hipStream_t>(stream)) != hipSuccess)
     return EXFOLD_ERR_DEVICE;
   return EXFOLD_OK;
 }
@@ -314,8 +324,9 @@ exfold_status exfold_select_decode_pool(const float *logits, int64_t B, int64_t 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int dd = (int)(D > N ? N : D);
   if (logits && B > 0) {
-    if (launch_route_tokens(logits, (int)B, (int)N, (int)K, (int)K, nullptr, nullptr, nullptr,
-                            topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s) != hipSuccess)
+    if (launch_route_tokens(logits, 1, nullptr, nullptr, (int)B, (int)N, (int)K, (int)K, nullptr,
+                            nullptr, nullptr, topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr,
+                            s) != hipSuccess)
       return EXFOLD_ERR_DEVICE;
   }
   if (launch_decode_pool_fold(topk_ids, topk_w, (int)B, (int)N, (int)K, dd, h, nullptr, nullptr,
@@ -341,7 +352,7 @@ exfold_status exfold_fold_gates(int32_t phase, int64_t T, int64_t N, int64_t K, 
     if (T == 0) return EXFOLD_OK;
     if (!topk_ids || !topk_w || !keep || !out_ids || !out_w) return EXFOLD_ERR_NULL;
     const int kp = (int)(budget > K ? K : budget);
-    if (launch_route_tokens(nullptr, (int)T, (int)N, (int)K, kp, nullptr, S, L,
+    if (launch_route_tokens(nullptr, 0, nullptr, nullptr, (int)T, (int)N, (int)K, kp, nullptr, S, L,
                             const_cast<int32_t *>(topk_ids), const_cast<float *>(topk_w), nullptr,
                             keep, out_ids, out_w, s) != hipSuccess)
       return EXFOLD_ERR_DEVICE;
@@ -382,7 +393,7 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
   hipStream_t s = static_cast<hipStream_t>(stream);
   const exfold_debug z{};
   const exfold_debug &dbg = debug ? *debug : z;
-  float *logits = dbg.logits ? dbg.logits : at<float>(ws, p.o_logits);
+  float *part = at<float>(ws, p.o_logits);
   int32_t *topk_ids = dbg.topk_ids ? dbg.topk_ids : at<int32_t>(ws, p.o_topk_ids);
   float *topk_w = dbg.topk_w ? dbg.topk_w : at<float>(ws, p.o_topk_w);
   uint8_t *keep = dbg.keep ? dbg.keep : at<uint8_t>(ws, p.o_keep);
@@ -392,33 +403,43 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
   float *fold_w = dbg.fold_w ? dbg.fold_w : at<float>(ws, p.o_fold_w);
 
   record(dbg.events, EXFOLD_EV_START, s);
-  if (launch_router_logits(layer->dtype, x, layer->w_router, layer->router_bias, p.T, p.N,
-                           (int)layer->d, logits, s) != hipSuccess)
+  if (launch_router_logits(layer->dtype, x, layer->w_router, p.T, p.N, (int)layer->d, p.P, part, s) !=
+      hipSuccess)
     return EXFOLD_ERR_DEVICE;
   record(dbg.events, EXFOLD_EV_ROUTER, s);
   const int32_t *exec_ids = fold_ids;
   const float *exec_w = fold_w;
+  const float *bias = layer->router_bias;
+  bool permuted = false;
   hipError_t e = hipSuccess;
   if (phase == EXFOLD_PHASE_DENSE) {
-    e = launch_route_tokens(logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr, topk_ids, topk_w,
-                            nullptr, nullptr, nullptr, nullptr, s);
+    e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,
+                            topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s);
     exec_ids = topk_ids;
     exec_w = topk_w;
   } else if (phase == EXFOLD_PHASE_PREFILL) {
-    e = launch_route_tokens(logits, p.T, p.N, p.K, p.k_out, tables->h, tables->S, tables->L,
-                            topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s);
+    e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.k_out, tables->h, tables->S,
+                            tables->L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s);
   } else {
-    e = launch_route_tokens(logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr, topk_ids, topk_w,
-                            nullptr, nullptr, nullptr, nullptr, s);
-    if (e == hipSuccess)
+    e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,
+                            topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s);
+    if (e == hipSuccess && (int64_t)p.T * p.K <= kDecodeFrontMaxSlots) {
+      // pool, tables, remap and permutation in one workgroup
+      const PermBuffers pb = perm_buffers(p.ex, ws, dbg.offsets, dbg.row_slot);
+      e = launch_decode_front(topk_ids, topk_w, p.T, p.N, p.K, p.dcap, tables->h, tables->S, tables->L,
+                              pool, pool_size, fold_ids, fold_w, dbg.tgt_ids, dbg.tgt_scale,
+                              p.ex.t_shared, p.ex.gu.bm, p.ex.dn.bm, pb, s);
+      permuted = true;
+    } else if (e == hipSuccess) {
       e = launch_decode_pool_fold(topk_ids, topk_w, p.T, p.N, p.K, p.dcap, tables->h, tables->S,
                                   tables->L, true, pool, pool_size, fold_ids, fold_w, dbg.tgt_ids,
                                   dbg.tgt_scale, s);
+    }
   }
   if (e != hipSuccess) return EXFOLD_ERR_DEVICE;
   record(dbg.events, EXFOLD_EV_FOLD, s);
   return run_exec(layer, p.ex, x, exec_ids, exec_w, y, ws, dbg.offsets, dbg.row_slot, false, s,
-                  dbg.events);
+                  dbg.events, permuted);
 }
 
 size_t exfold_execute_workspace_size(const exfold_layer *layer, int64_t T, int64_t k_out) {
@@ -471,11 +492,12 @@ exfold_status exfold_calibrate_projectors(const exfold_layer *layer, const void 
   int16_t *pos = at<int16_t>(ws, p.o_pos);
   double *gram = at<double>(ws, p.o_gram);
   if (p.m > 0) {
-    if (launch_router_logits(layer->dtype, x_cal, layer->w_router, layer->router_bias, p.m, p.N,
-                             (int)layer->d, logits, s) != hipSuccess)
+    if (launch_router_logits(layer->dtype, x_cal, layer->w_router, p.m, p.N, (int)layer->d, p.P,
+                             logits, s) != hipSuccess)
       return EXFOLD_ERR_DEVICE;
-    if (launch_route_tokens(logits, p.m, p.N, p.K, p.K, nullptr, nullptr, nullptr, topk_ids, topk_w,
-                            nullptr, nullptr, nullptr, nullptr, s) != hipSuccess)
+    if (launch_route_tokens(logits, p.P, layer->router_bias, nullptr, p.m, p.N, p.K, p.K, nullptr,
+                            nullptr, nullptr, topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr,
+                            s) != hipSuccess)
       return EXFOLD_ERR_DEVICE;
     if (launch_calib_routes(topk_ids, p.m, p.N, p.K, mode, route_ids, route_w, pos, s) != hipSuccess)
       return EXFOLD_ERR_DEVICE;

@@ -468,9 +468,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
                                                      int rows, const int32_t *__restrict__ slot_row,
                                                      int k_out, int d, int shared_base,
                                                      OutT *__restrict__ y) {
+  // block (i, c): token i, columns [1024 c, 1024 c + 1024), four per thread
   const int i = blockIdx.x;
   const long long split = (long long)rows * d;
-  for (int c = threadIdx.x * 4; c < d; c += 256 * 4) {
+  for (int c = blockIdx.y * 1024 + threadIdx.x * 4; c < min(d, (int)(blockIdx.y + 1) * 1024); c += 1024) {
     float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int k = 0; k <= k_out; ++k) {
       long long r;
@@ -496,12 +497,13 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
 hipError_t launch_combine(int dtype, const float *Y, int ksplit, int rows, const int32_t *slot_row,
                           int T, int k_out, int d, int shared_base, void *y, hipStream_t s) {
   if (T <= 0) return hipSuccess;
+  const dim3 grid(T, (d + 1023) / 1024);
   if (dtype == EXFOLD_BF16)
-    combine_kernel<bf16_t><<<T, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
-                                             static_cast<bf16_t *>(y));
+    combine_kernel<bf16_t><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
+                                                static_cast<bf16_t *>(y));
   else
-    combine_kernel<float><<<T, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
-                                            static_cast<float *>(y));
+    combine_kernel<float><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
+                                               static_cast<float *>(y));
   return hipGetLastError();
 }
 

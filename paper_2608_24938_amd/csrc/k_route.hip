@@ -15,22 +15,26 @@
 namespace exfold {
 
 // ---------------------------------------------------------------------------
-// Router logits.  bf16: a workgroup of KS waves takes 16 tokens; wave w reduces
-// its slice of d with 16x16x32 bf16 MFMA against all NT*16 (padded) experts, and
-// the KS partial sums are added in a fixed order through LDS.  W_r stays in L2.
+// Router logits, as P partial sums over slices of d (the bias and the sum of the
+// partials are taken by the Top-K kernel, in a fixed order).  bf16: workgroup
+// (bx, by, bz) takes 16 tokens x NT*16 experts x one d-slice; its KS waves split
+// the slice, reduce with 16x16x32 bf16 MFMA and add their partial sums in a fixed
+// order through LDS.  Many tokens: one block covers every expert (W_r is read
+// once per 16 tokens); few tokens: 16 experts per block and the d axis split
+// over the grid, so the small GEMM still spreads over the CUs.
 // f32: one thread per logit.
 // ---------------------------------------------------------------------------
 template <int NT, int KS>
 __global__ __launch_bounds__(64 * KS) void router_logits_bf16(const bf16_t *__restrict__ x,
                                                               const bf16_t *__restrict__ wr,
-                                                              const float *__restrict__ bias,
-                                                              int T, int N, int d,
-                                                              float *__restrict__ logits) {
+                                                              int T, int N, int d, int d_slice,
+                                                              float *__restrict__ part) {
   __shared__ float red[KS][NT * 4][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
   const int t0 = blockIdx.x * 16;
+  const int e0 = blockIdx.y * NT * 16;
   const int row = min(t0 + (lane & 15), T - 1);
-  const int kq = (lane >> 4) * 8;
+  const int kq = (lane >> 4) * 8 + blockIdx.z * d_slice;
   f32x4 acc[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -38,12 +42,12 @@ __global__ __launch_bounds__(64 * KS) void router_logits_bf16(const bf16_t *__re
   bool live[NT];
 #pragma unroll
   for (int j = 0; j < NT; ++j) {
-    const int e = j * 16 + (lane & 15);
+    const int e = e0 + j * 16 + (lane & 15);
     live[j] = e < N;
     wrow[j] = wr + (size_t)(live[j] ? e : 0) * d + kq;
   }
   const bf16_t *xa = x + (size_t)row * d + kq;
-  const int steps = d / 32;
+  const int steps = d_slice / 32;
   const int s0 = wave * steps / KS, s1 = (wave + 1) * steps / KS;
   bf16x8 zero;
 #pragma unroll
@@ -79,7 +83,8 @@ __global__ __launch_bounds__(64 * KS) void router_logits_bf16(const bf16_t *__re
 #pragma unroll
     for (int i = 0; i < 4; ++i) red[wave][j * 4 + i][lane] = acc[j][i];
   __syncthreads();
-  // entry (j, i, l): expert j*16 + l%16, token t0 + (l/16)*4 + i
+  // entry (j, i, l): expert e0 + j*16 + l%16, token t0 + (l/16)*4 + i
+  float *out = part + (size_t)blockIdx.z * T * N;
   for (int idx = threadIdx.x; idx < NT * 4 * 64; idx += 64 * KS) {
     const int ji = idx >> 6, l = idx & 63;
     const int j = ji >> 2, i = ji & 3;
@@ -87,25 +92,38 @@ __global__ __launch_bounds__(64 * KS) void router_logits_bf16(const bf16_t *__re
 #pragma unroll
     for (int w = 1; w < KS; ++w) v += red[w][ji][l];
     const int t = t0 + (l >> 4) * 4 + i;
-    const int e = j * 16 + (l & 15);
-    if (t < T && e < N) logits[(size_t)t * N + e] = v + (bias ? bias[e] : 0.0f);
+    const int e = e0 + j * 16 + (l & 15);
+    if (t < T && e < N) out[(size_t)t * N + e] = v;
   }
 }
 
+// Blocks of the all-experts layout at or above which the d axis is not split.
+constexpr int kRouterWideBlocks = 64;
+
+int router_splits(int dtype, int T, int N, int d) {
+  if (dtype != EXFOLD_BF16 || T <= 0) return 1;
+  const int tb = (T + 15) / 16;
+  if (tb >= kRouterWideBlocks) return 1;
+  const int nb = (N + 15) / 16;
+  int P = 1;
+  // split d (slices of >= 256, multiples of 32) until the grid covers ~256 CUs
+  while (tb * nb * P < 256 && d % (64 * P) == 0 && d / (2 * P) >= 256) P *= 2;
+  return P;
+}
+
 template <int NT>
-static void launch_router_nt(const bf16_t *x, const bf16_t *wr, const float *bias, int T, int N, int d,
-                             float *logits, hipStream_t s) {
+static void launch_router_wide(const bf16_t *x, const bf16_t *wr, int T, int N, int d, float *part,
+                               hipStream_t s) {
   const int blocks = (T + 15) / 16;
   if (blocks < 512)
-    router_logits_bf16<NT, 8><<<blocks, 512, 0, s>>>(x, wr, bias, T, N, d, logits);
+    router_logits_bf16<NT, 8><<<dim3(blocks, 1, 1), 512, 0, s>>>(x, wr, T, N, d, d, part);
   else
-    router_logits_bf16<NT, 4><<<blocks, 256, 0, s>>>(x, wr, bias, T, N, d, logits);
+    router_logits_bf16<NT, 4><<<dim3(blocks, 1, 1), 256, 0, s>>>(x, wr, T, N, d, d, part);
 }
 
 __global__ __launch_bounds__(256) void router_logits_f32(const float *__restrict__ x,
-                                                         const float *__restrict__ wr,
-                                                         const float *__restrict__ bias, int T,
-                                                         int N, int d, float *__restrict__ logits) {
+                                                         const float *__restrict__ wr, int T,
+                                                         int N, int d, float *__restrict__ part) {
   const int idx = blockIdx.x * blockDim.x + threadIdx.x;
   if (idx >= T * N) return;
   const int t = idx / N, e = idx % N;
@@ -113,24 +131,31 @@ __global__ __launch_bounds__(256) void router_logits_f32(const float *__restrict
   const float *wrow = wr + (size_t)e * d;
   float acc = 0.f;
   for (int k = 0; k < d; ++k) acc = fmaf(xr[k], wrow[k], acc);
-  logits[idx] = acc + (bias ? bias[e] : 0.0f);
+  part[idx] = acc;
 }
 
-hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, const float *bias,
-                                int T, int N, int d, float *logits, hipStream_t s) {
+hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, int T, int N, int d,
+                                int P, float *part, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   if (dtype == EXFOLD_BF16) {
     const bf16_t *xb = static_cast<const bf16_t *>(x);
     const bf16_t *wb = static_cast<const bf16_t *>(w_router);
-    const int nt = (N + 15) / 16;
-    if (nt <= 1) launch_router_nt<1>(xb, wb, bias, T, N, d, logits, s);
-    else if (nt <= 2) launch_router_nt<2>(xb, wb, bias, T, N, d, logits, s);
-    else if (nt <= 4) launch_router_nt<4>(xb, wb, bias, T, N, d, logits, s);
-    else if (nt <= 8) launch_router_nt<8>(xb, wb, bias, T, N, d, logits, s);
-    else launch_router_nt<16>(xb, wb, bias, T, N, d, logits, s);
+    const int tb = (T + 15) / 16;
+    if (tb < kRouterWideBlocks) {
+      // 16 tokens x 16 experts x d/P per block
+      const dim3 grid(tb, (N + 15) / 16, P);
+      router_logits_bf16<1, 4><<<grid, 256, 0, s>>>(xb, wb, T, N, d, d / P, part);
+    } else {
+      const int nt = (N + 15) / 16;
+      if (nt <= 1) launch_router_wide<1>(xb, wb, T, N, d, part, s);
+      else if (nt <= 2) launch_router_wide<2>(xb, wb, T, N, d, part, s);
+      else if (nt <= 4) launch_router_wide<4>(xb, wb, T, N, d, part, s);
+      else if (nt <= 8) launch_router_wide<8>(xb, wb, T, N, d, part, s);
+      else launch_router_wide<16>(xb, wb, T, N, d, part, s);
+    }
   } else {
     router_logits_f32<<<(T * N + 255) / 256, 256, 0, s>>>(
-        static_cast<const float *>(x), static_cast<const float *>(w_router), bias, T, N, d, logits);
+        static_cast<const float *>(x), static_cast<const float *>(w_router), T, N, d, part);
   }
   return hipGetLastError();
 }
@@ -140,15 +165,35 @@ hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, 
 // Lane k (< K) owns route k of the token.
 // ---------------------------------------------------------------------------
 
-// Top-K by (logit desc, id asc) over a row of N <= 256 logits; the softmax over
-// the selected logits is evaluated in float64 and rounded once to float32.
-__device__ __forceinline__ void wave_topk_softmax(const float *__restrict__ row, int N, int K,
-                                                  int lane, int &my_id, float &my_w) {
+// Logit row of token t: the P partial sums in order, then the bias; lane holds
+// experts lane + 64 j.  The row is also written to `out` when given.
+__device__ __forceinline__ void wave_logit_row(const float *__restrict__ part, int P, int T, int N,
+                                               const float *__restrict__ bias, int t, int lane,
+                                               float *__restrict__ out, float v[4]) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const int e = lane + 64 * j;
+    float a = 0.f;
+    if (e < N) {
+      a = part[(size_t)t * N + e];
+      for (int z = 1; z < P; ++z) a += part[((size_t)z * T + t) * N + e];
+      if (bias) a += bias[e];
+      if (out) out[(size_t)t * N + e] = a;
+    }
+    v[j] = a;
+  }
+}
+
+// Top-K by (logit desc, id asc) over a row of N <= 256 logits (lane holds
+// experts lane + 64 j); the softmax over the selected logits is evaluated in
+// float64 and rounded once to float32.
+__device__ __forceinline__ void wave_topk_softmax(const float v[4], int N, int K, int lane,
+                                                  int &my_id, float &my_w) {
   uint64_t key[4];
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + 64 * j;
-    key[j] = (e < N) ? ((uint64_t(float_key(row[e])) << 32) | uint64_t(0xffffffffu - uint32_t(e))) : 0ull;
+    key[j] = (e < N) ? ((uint64_t(float_key(v[j])) << 32) | uint64_t(0xffffffffu - uint32_t(e))) : 0ull;
   }
   my_id = 0;
   for (int k = 0; k < K; ++k) {
@@ -163,7 +208,11 @@ __device__ __forceinline__ void wave_topk_softmax(const float *__restrict__ row,
       if (lane + 64 * j == id) key[j] = 0ull;
   }
   my_id = clamp_id(my_id, N);
-  const double r = (double)row[my_id];
+  // logit of my route: held by lane my_id % 64 in register my_id / 64
+  const int src = my_id & 63, reg = my_id >> 6;
+  const float c0 = __shfl(v[0], src, kWave), c1 = __shfl(v[1], src, kWave);
+  const float c2 = __shfl(v[2], src, kWave), c3 = __shfl(v[3], src, kWave);
+  const double r = (double)(reg == 0 ? c0 : reg == 1 ? c1 : reg == 2 ? c2 : c3);
   const double r0 = shfl_f64(r, 0);  // route 0 holds the largest logit
   double z = (lane < K) ? exp(r - r0) : 0.0;
   double sum = z;
@@ -173,7 +222,8 @@ __device__ __forceinline__ void wave_topk_softmax(const float *__restrict__ row,
 }
 
 __global__ __launch_bounds__(256) void route_tokens_kernel(
-    const float *__restrict__ logits, int T, int N, int K, int k_pre, const float *__restrict__ h,
+    const float *__restrict__ part, int P, const float *__restrict__ bias,
+    float *__restrict__ logits_out, int T, int N, int K, int k_pre, const float *__restrict__ h,
     const float *__restrict__ S, const float *__restrict__ L, int32_t *__restrict__ topk_ids,
     float *__restrict__ topk_w, uint8_t *__restrict__ keep, const uint8_t *__restrict__ keep_in,
     int32_t *__restrict__ fold_ids, float *__restrict__ fold_w) {
@@ -182,8 +232,10 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   if (t >= T) return;  // uniform per wave
   int my_id = 0;
   float my_w = 0.f;
-  if (logits) {
-    wave_topk_softmax(logits + (size_t)t * N, N, K, lane, my_id, my_w);
+  if (part) {
+    float v[4];
+    wave_logit_row(part, P, T, N, bias, t, lane, logits_out, v);
+    wave_topk_softmax(v, N, K, lane, my_id, my_w);
     if (lane < K) {
       topk_ids[(size_t)t * K + lane] = my_id;
       topk_w[(size_t)t * K + lane] = my_w;
@@ -253,13 +305,14 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   }
 }
 
-hipError_t launch_route_tokens(const float *logits, int T, int N, int K, int k_pre, const float *h,
-                               const float *S, const float *L, int32_t *topk_ids, float *topk_w,
-                               uint8_t *keep, const uint8_t *keep_in, int32_t *fold_ids,
-                               float *fold_w, hipStream_t s) {
+hipError_t launch_route_tokens(const float *part, int P, const float *bias, float *logits_out, int T,
+                               int N, int K, int k_pre, const float *h, const float *S, const float *L,
+                               int32_t *topk_ids, float *topk_w, uint8_t *keep,
+                               const uint8_t *keep_in, int32_t *fold_ids, float *fold_w,
+                               hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  route_tokens_kernel<<<(T + 3) / 4, 256, 0, s>>>(logits, T, N, K, k_pre, h, S, L, topk_ids, topk_w,
-                                                  keep, keep_in, fold_ids, fold_w);
+  route_tokens_kernel<<<(T + 3) / 4, 256, 0, s>>>(part, P, bias, logits_out, T, N, K, k_pre, h, S, L,
+                                                  topk_ids, topk_w, keep, keep_in, fold_ids, fold_w);
   return hipGetLastError();
 }
 
@@ -365,6 +418,272 @@ __global__ __launch_bounds__(kPoolThreads) void decode_pool_fold_kernel(
     out_ids[j] = tgt[e];
     out_w[j] = in_pool[e] ? wv : wv * scl[e];
   }
+}
+
+// ---------------------------------------------------------------------------
+// Decode front end in one workgroup, after the per-token Top-K: the batch pool,
+// the per-source tables, the remap of every slot and the stable permutation of
+// the remapped slots by expert (the same outputs as the separate pool/fold and
+// permutation kernels), so a decode step launches one kernel between Top-K and
+// the expert GEMMs.  The [B, K] slots stay in LDS after one read.
+// ---------------------------------------------------------------------------
+constexpr int kFrontWaves = kPoolThreads / kWave;
+
+__global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
+    const int32_t *__restrict__ ids, const float *__restrict__ w, int B, int N, int K, int D,
+    const float *__restrict__ h, const float *__restrict__ S, const float *__restrict__ L,
+    int32_t *__restrict__ pool_g, int32_t *__restrict__ pool_size_g, int32_t *__restrict__ out_ids,
+    float *__restrict__ out_w, int32_t *__restrict__ tgt_g, float *__restrict__ scl_g, int t_shared,
+    int bm0, int bm1, int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start0,
+    int32_t *__restrict__ tile_start1, int32_t *__restrict__ row_token,
+    int32_t *__restrict__ row_slot, float *__restrict__ row_w, int32_t *__restrict__ slot_row) {
+  __shared__ uint8_t sid[kDecodeFrontMaxSlots];   // expert of each slot (N <= 256)
+  __shared__ float sw[kDecodeFrontMaxSlots];      // its weight
+  __shared__ unsigned long long wsum[kMaxExperts];
+  __shared__ int cnt[kMaxExperts];
+  __shared__ double score[kMaxExperts];
+  __shared__ int pool[kMaxExperts];
+  __shared__ int in_pool[kMaxExperts];
+  __shared__ int tgt[kMaxExperts];
+  __shared__ float scl[kMaxExperts];
+  __shared__ int rows_of[kMaxExperts];  // executed rows per routed expert
+  __shared__ int rank_sh[kMaxExperts];
+  __shared__ int cur[kMaxExperts];
+  __shared__ int wcnt[kFrontWaves][kMaxExperts];
+  __shared__ int n_pool;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int slots = B * K;
+  const int dcap = min(D, N);
+  const int groups = N + (t_shared > 0 ? 1 : 0);
+
+  const float h_e = (tid < N) ? h[tid] : 0.f;
+  if (tid < N) {
+    wsum[tid] = 0ull;
+    cnt[tid] = 0;
+    in_pool[tid] = 0;
+    rows_of[tid] = 0;
+    rank_sh[tid] = 0;
+  }
+  __syncthreads();
+
+  // ---- pool (Eq. decode_budget): exact fixed-point weight sums ----
+  for (int j = tid; j < slots; j += kPoolThreads) {
+    const int e = clamp_id(ids[j], N);
+    const float wv = w[j];
+    sid[j] = (uint8_t)e;
+    sw[j] = wv;
+    const long long q = __double2ll_rn((double)wv * 1099511627776.0);  // 2^40
+    atomicAdd(&wsum[e], (unsigned long long)q);
+    atomicAdd(&cnt[e], 1);
+  }
+  __syncthreads();
+  if (tid < N) score[tid] = (double)(long long)wsum[tid] * (double)h_e;
+  const int n_cand = __syncthreads_count(tid < N && cnt[tid] > 0);
+  // rank of each candidate by (score desc, id asc): thread (e, part) compares e
+  // with one slice of the experts; the integer partial ranks add in any order
+  {
+    const int parts = kPoolThreads / N;
+    const int e = tid % N, pt = tid / N;
+    if (pt < parts) {
+      const int chunk = (N + parts - 1) / parts;
+      const int lo = pt * chunk, hi = min(N, lo + chunk);
+      const double sc = score[e];
+      int my = 0;
+#pragma unroll 8
+      for (int o = lo; o < hi; ++o)
+        my += (cnt[o] > 0) && ((score[o] > sc) || (score[o] == sc && o < e));
+      atomicAdd(&rank_sh[e], my);
+    }
+  }
+  __syncthreads();
+  if (tid < N && cnt[tid] > 0 && rank_sh[tid] < dcap) {
+    pool[rank_sh[tid]] = tid;
+    in_pool[tid] = 1;
+  }
+  if (tid == 0) n_pool = min(dcap, n_cand);
+  __syncthreads();
+  if (tid < dcap) pool_g[tid] = (tid < n_pool) ? pool[tid] : -1;
+  if (tid == 0) *pool_size_g = n_pool;
+
+  // ---- per-source tables (Eq. minimum_loss_assignment over the pool) ----
+  // Wave w takes sources w + 16 u; lane l reads L[s, pool[l + 64 c]] and
+  // S[s, pool[l + 64 c]] (eight sources per batch, so 16 loads are in flight)
+  // and the wave keeps the first minimum in pool order (64-bit key: value,
+  // index) together with its scale.
+  for (int base = wave; base < N; base += kFrontWaves * 8) {
+    uint64_t best[8];
+    float bs[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      best[u] = ~0ull;
+      bs[u] = 1.0f;
+    }
+    for (int c = 0; c < n_pool; c += kWave) {
+      const int j = c + lane;
+      const bool live = j < n_pool;
+      const int pj = live ? pool[j] : 0;
+      float lv[8], sv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const size_t o = (size_t)min(base + kFrontWaves * u, N - 1) * N + pj;
+        lv[u] = L[o];
+        sv[u] = S[o];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint64_t key = live ? ((uint64_t(float_key(lv[u])) << 32) | uint64_t(j)) : ~0ull;
+        if (key < best[u]) {
+          best[u] = key;
+          bs[u] = sv[u];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int src = base + kFrontWaves * u;
+      uint64_t b = best[u];
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const uint64_t o = shfl_xor_u64(b, m);
+        b = o < b ? o : b;
+      }
+      // the lane holding the minimum (keys are distinct: they carry the index)
+      const uint64_t holder = __ballot(best[u] == b);
+      const float s_min = __shfl(bs[u], holder ? (int)__ffsll((long long)holder) - 1 : 0, kWave);
+      if (src < N && lane == 0) {
+        int t_best = src;
+        float s_best = 1.0f;
+        if (!in_pool[src] && n_pool > 0) {
+          t_best = pool[(int)(b & 0xffffffffu)];
+          s_best = s_min;
+        }
+        tgt[src] = t_best;
+        scl[src] = s_best;
+        if (tgt_g) tgt_g[src] = t_best;
+        if (scl_g) scl_g[src] = s_best;
+      }
+    }
+  }
+  __syncthreads();
+
+  // ---- remap every slot (Eq. decode_remap); retained slots copied ----
+  for (int j = tid; j < slots; j += kPoolThreads) {
+    const int e = sid[j];
+    const float wv = sw[j];
+    const int te = tgt[e];
+    const float wn = in_pool[e] ? wv : wv * scl[e];
+    out_ids[j] = te;
+    out_w[j] = wn;
+    sid[j] = (uint8_t)te;
+    sw[j] = wn;
+    atomicAdd(&rows_of[te], 1);
+  }
+  __syncthreads();
+
+  // ---- group offsets and GEMM m-tile lists: wave 0, five groups per lane ----
+  if (wave == 0) {
+    constexpr int G = 5;  // 64 * 5 >= kMaxExperts + 1 groups
+    int r[G], a[G], b[G];
+    int sr = 0, sa = 0, sb = 0;
+#pragma unroll
+    for (int q = 0; q < G; ++q) {
+      const int g = lane * G + q;
+      r[q] = (g < N) ? rows_of[g] : (g == N && g < groups) ? t_shared : 0;
+      a[q] = g < groups ? (r[q] + bm0 - 1) / bm0 : 0;
+      b[q] = g < groups ? (r[q] + bm1 - 1) / bm1 : 0;
+      sr += r[q];
+      sa += a[q];
+      sb += b[q];
+    }
+    // exclusive prefix over lanes
+    int er = sr, ea = sa, eb = sb;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+      const int xr = __shfl_up(er, off, kWave), xa = __shfl_up(ea, off, kWave), xb = __shfl_up(eb, off, kWave);
+      if (lane >= off) {
+        er += xr;
+        ea += xa;
+        eb += xb;
+      }
+    }
+    er -= sr;
+    ea -= sa;
+    eb -= sb;
+    const int ta = __shfl(ea + sa, kWave - 1, kWave), tb = __shfl(eb + sb, kWave - 1, kWave);
+#pragma unroll
+    for (int q = 0; q < G; ++q) {
+      const int g = lane * G + q;
+      if (g < N) cur[g] = er;  // group start (routed experts)
+      if (g < N + 2) {
+        offsets[g] = (g < N) ? er : (g == N) ? slots : slots + t_shared;
+        tile_start0[g] = (g < groups) ? ea : ta;
+        tile_start1[g] = (g < groups) ? eb : tb;
+      }
+      er += r[q];
+      ea += a[q];
+      eb += b[q];
+    }
+  }
+  for (int e = tid; e < N; e += kPoolThreads) {
+#pragma unroll
+    for (int q = 0; q < kFrontWaves; ++q) wcnt[q][e] = 0;
+  }
+  __syncthreads();
+
+  // ---- stable scatter: rounds of kPoolThreads slots in slot order ----
+  for (int base = 0; base < slots; base += kPoolThreads) {
+    const int j = base + tid;
+    const bool valid = j < slots;
+    const int e = valid ? (int)sid[j] : 0;
+    // lanes of this wave with the same expert (8 ballots: N <= 256)
+    uint64_t m = __ballot(valid);
+#pragma unroll
+    for (int bit = 0; bit < 8; ++bit) {
+      const bool set = (e >> bit) & 1;
+      const uint64_t bal = __ballot(set);
+      m &= set ? bal : ~bal;
+    }
+    const int rank = __popcll(m & lanemask_lt(lane));
+    if (valid && rank == 0) wcnt[wave][e] = __popcll(m);
+    __syncthreads();
+    if (valid) {
+      int pos = cur[e] + rank;
+      for (int q = 0; q < wave; ++q) pos += wcnt[q][e];
+      row_slot[pos] = j;
+      row_token[pos] = j / K;
+      row_w[pos] = sw[j];
+      slot_row[j] = pos;
+    }
+    __syncthreads();
+    for (int x = tid; x < N; x += kPoolThreads) {
+      int add = 0;
+#pragma unroll
+      for (int q = 0; q < kFrontWaves; ++q) {
+        add += wcnt[q][x];
+        wcnt[q][x] = 0;
+      }
+      cur[x] += add;
+    }
+    __syncthreads();
+  }
+  // Shared-expert rows follow the routed rows, one per token, weight 1.
+  for (int i = tid; i < t_shared; i += kPoolThreads) {
+    row_token[slots + i] = i;
+    row_slot[slots + i] = -1;
+    row_w[slots + i] = 1.0f;
+  }
+}
+
+hipError_t launch_decode_front(const int32_t *ids, const float *w, int B, int N, int K, int D,
+                               const float *h, const float *S, const float *L, int32_t *pool,
+                               int32_t *pool_size, int32_t *out_ids, float *out_w, int32_t *tgt,
+                               float *scl, int t_shared, int bm0, int bm1, const PermBuffers &pb,
+                               hipStream_t s) {
+  decode_front_kernel<<<1, kPoolThreads, 0, s>>>(ids, w, B, N, K, D, h, S, L, pool, pool_size, out_ids,
+                                                 out_w, tgt, scl, t_shared, bm0, bm1, pb.offsets,
+                                                 pb.tile_start0, pb.tile_start1, pb.row_token,
+                                                 pb.row_slot, pb.row_w, pb.slot_row);
+  return hipGetLastError();
 }
 
 hipError_t launch_decode_pool_fold(const int32_t *ids, const float *w, int B, int N, int K, int D,

@@ -8,14 +8,18 @@
 namespace exfold {
 
 // ---- routing (k_route.hip) ----
-hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, const float *bias,
-                                int T, int N, int d, float *logits, hipStream_t s);
-// Per-token Top-K + softmax (if logits != nullptr), prefill selection (if keep
-// or fold outputs are requested) and prefill fold (if fold_ids != nullptr).
-hipError_t launch_route_tokens(const float *logits, int T, int N, int K, int k_pre, const float *h,
-                               const float *S, const float *L, int32_t *topk_ids, float *topk_w,
-                               uint8_t *keep, const uint8_t *keep_in, int32_t *fold_ids,
-                               float *fold_w, hipStream_t s);
+hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, int T, int N, int d,
+                                int P, float *part, hipStream_t s);
+// Number of d-slices (partial sums) the router uses for T tokens: [P, T, N] floats.
+int router_splits(int dtype, int T, int N, int d);
+// Per-token Top-K + softmax (if part != nullptr: logits = sum of the P partials
+// + bias, written to logits_out if given), prefill selection (if keep or fold
+// outputs are requested) and prefill fold (if fold_ids != nullptr).
+hipError_t launch_route_tokens(const float *part, int P, const float *bias, float *logits_out, int T,
+                               int N, int K, int k_pre, const float *h, const float *S, const float *L,
+                               int32_t *topk_ids, float *topk_w, uint8_t *keep,
+                               const uint8_t *keep_in, int32_t *fold_ids, float *fold_w,
+                               hipStream_t s);
 // Decode pool (if do_pool) and per-source tables + per-slot remap (if out_ids).
 hipError_t launch_decode_pool_fold(const int32_t *ids, const float *w, int B, int N, int K, int D,
                                    const float *h, const float *S, const float *L, bool do_pool,
@@ -38,6 +42,15 @@ struct PermBuffers {
 // shared-expert rows are appended after the routed rows.
 hipError_t launch_permute(const int32_t *route_ids, const float *route_w, int T, int k_out, int N,
                           int t_shared, int bm0, int bm1, const PermBuffers &pb, hipStream_t s);
+// Decode front end in one workgroup, after Top-K: pool, tables, remap and the
+// permutation of the remapped [B, K] slots (pb.blk_counts unused).  For
+// B * K <= kDecodeFrontMaxSlots.
+constexpr int kDecodeFrontMaxSlots = 8192;
+hipError_t launch_decode_front(const int32_t *ids, const float *w, int B, int N, int K, int D,
+                               const float *h, const float *S, const float *L, int32_t *pool,
+                               int32_t *pool_size, int32_t *out_ids, float *out_w, int32_t *tgt,
+                               float *scl, int t_shared, int bm0, int bm1, const PermBuffers &pb,
+                               hipStream_t s);
 
 // ---- expert GEMMs and combine (k_gemm.hip) ----
 enum { kGemmSimt = 0, kGemmTile = 1 };
