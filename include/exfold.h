@@ -67,7 +67,10 @@ enum { EXFOLD_F32 = 0, EXFOLD_BF16 = 1 };
 enum {
   EXFOLD_PHASE_DENSE = 0,    /* unfolded layer on the Top-K routes (Eq. moe_output)  */
   EXFOLD_PHASE_PREFILL = 1,  /* per-token K' budget (Eq. prefill_budget/prefill_fold) */
-  EXFOLD_PHASE_DECODE = 2    /* per-batch pool of D (Eq. decode_budget/decode_remap)  */
+  EXFOLD_PHASE_DECODE = 2,   /* per-batch pool of D (Eq. decode_budget/decode_remap)  */
+  EXFOLD_PHASE_DECODE_STATIC = 3  /* static pool of D: remap with precomputed tables
+                                     (Appendix B, Eq. appendix_decode_static_budget,
+                                     Eq. appendix_decode_remap); see exfold_static_pool */
 };
 
 enum {
@@ -93,11 +96,15 @@ typedef struct exfold_layer {
 } exfold_layer;
 
 /* Calibrated per-layer tables (Sec. 4.2): S[s*N+t] = s*_{s->t}, L[s*N+t] = l_{s->t}
- * (row = source s, column = target t), h[e] = output-norm estimate of expert e. */
+ * (row = source s, column = target t), h[e] = output-norm estimate of expert e.
+ * tgt/scl: the per-source tables of a static decode pool (exfold_static_pool);
+ * required by EXFOLD_PHASE_DECODE_STATIC, ignored (may be NULL) otherwise. */
 typedef struct exfold_tables {
-  const float *S;  /* [N, N] float32 */
-  const float *L;  /* [N, N] float32 */
-  const float *h;  /* [N]    float32 */
+  const float *S;      /* [N, N] float32 */
+  const float *L;      /* [N, N] float32 */
+  const float *h;      /* [N]    float32 */
+  const int32_t *tgt;  /* [N]    int32: target of each source expert, or NULL */
+  const float *scl;    /* [N]    float32: its scale, or NULL                  */
 } exfold_tables;
 
 /* Stage boundaries at which exfold_moe_forward records the optional events. */
@@ -184,6 +191,23 @@ exfold_status exfold_fold_gates(int32_t phase, int64_t T, int64_t N, int64_t K, 
                                 int32_t *out_ids, float *out_w, int32_t *tgt_ids,
                                 float *tgt_scale, void *stream);
 
+/*
+ * Static decode pool (Appendix B, Eq. appendix_decode_static_budget): formed
+ * once from the calibration norms, independent of the batch.
+ *   h         [N] float32 output-norm estimates.
+ *   pool      [min(D, N)] int32 output: the D experts of largest h in (h desc,
+ *             id asc) order.  pool_size [1] int32 output: min(D, N).
+ *   tgt, scl  [N] outputs: the per-source tables of this pool (a source in the
+ *             pool maps to itself with scale 1; any other source s to the first
+ *             minimum t of L[s, t] over the pool in pool order, with scale
+ *             S[s, t]).  Pass them as exfold_tables.tgt/scl to an
+ *             EXFOLD_PHASE_DECODE_STATIC forward, whose per-step fold is then
+ *             one lookup per routed slot (Eq. appendix_decode_remap).
+ */
+exfold_status exfold_static_pool(const float *h, int64_t N, int64_t D, const float *S,
+                                 const float *L, int32_t *pool, int32_t *pool_size, int32_t *tgt,
+                                 float *scl, void *stream);
+
 /* Bytes of workspace exfold_moe_forward needs for T tokens, or 0 on invalid input. */
 size_t exfold_moe_workspace_size(const exfold_layer *layer, int64_t T, int32_t phase,
                                  int64_t budget);
@@ -194,6 +218,9 @@ size_t exfold_moe_workspace_size(const exfold_layer *layer, int64_t T, int32_t p
  * grouped SwiGLU expert GEMMs over the retained routes only, weighted combine.
  *   x   [T, d] input tokens, y [T, d] output (same dtype as the layer).
  *   tables may be NULL for EXFOLD_PHASE_DENSE; budget is ignored there.
+ *   EXFOLD_PHASE_DECODE_STATIC needs tables->tgt/scl from exfold_static_pool
+ *   (budget = its D) and leaves the debug pool/pool_size/tgt_ids/tgt_scale
+ *   untouched; a slot of source s becomes (tgt[s], w * scl[s]) unless tgt[s] == s.
  *   y_i = sum over executed routes (e, w) of w * E_e(x_i), plus the shared
  *   expert with weight 1; float32 accumulation, one rounding to the dtype.
  *   debug may be NULL.  ws/ws_bytes: workspace of at least

@@ -189,7 +189,8 @@ exfold_status plan_forward(const exfold_layer *L, int64_t T, int32_t phase, int6
                            ForwardPlan &p) {
   exfold_status st = check_layer(L);
   if (st != EXFOLD_OK) return st;
-  if (phase != EXFOLD_PHASE_DENSE && phase != EXFOLD_PHASE_PREFILL && phase != EXFOLD_PHASE_DECODE)
+  if (phase != EXFOLD_PHASE_DENSE && phase != EXFOLD_PHASE_PREFILL && phase != EXFOLD_PHASE_DECODE &&
+      phase != EXFOLD_PHASE_DECODE_STATIC)
     return EXFOLD_ERR_ARG;
   st = check_routing(T, L->n_experts, L->top_k);
   if (st != EXFOLD_OK) return st;
@@ -214,7 +215,7 @@ exfold_status plan_forward(const exfold_layer *L, int64_t T, int32_t phase, int6
   p.o_fold_ids = c.take(sizeof(int32_t) * (size_t)p.T * p.k_out);
   p.o_fold_w = c.take(sizeof(float) * (size_t)p.T * p.k_out);
   int active = p.N;
-  if (phase == EXFOLD_PHASE_DECODE) active = p.dcap;
+  if (phase == EXFOLD_PHASE_DECODE || phase == EXFOLD_PHASE_DECODE_STATIC) active = p.dcap;
   if (p.T * p.k_out < active) active = p.T * p.k_out;
   if (L->shared_inter > 0) active += 1;
   plan_exec(L, phase, p.T, p.k_out, true, false, active, c, p.ex);
@@ -336,6 +337,20 @@ exfold_status exfold_select_decode_pool(const float *logits, int64_t B, int64_t 
   return EXFOLD_OK;
 }
 
+exfold_status exfold_static_pool(const float *h, int64_t N, int64_t D, const float *S,
+                                 const float *L, int32_t *pool, int32_t *pool_size, int32_t *tgt,
+                                 float *scl, void *stream) {
+  if (N <= 0) return EXFOLD_ERR_SHAPE;
+  if (N > kMaxExperts) return EXFOLD_ERR_UNSUPPORTED;
+  if (D < 1) return EXFOLD_ERR_BUDGET;
+  if (!h || !S || !L || !pool || !pool_size || !tgt || !scl) return EXFOLD_ERR_NULL;
+  const int dd = (int)(D > N ? N : D);
+  if (launch_static_pool(h, (int)N, dd, S, L, pool, pool_size, tgt, scl,
+                         static_cast<hipStream_t>(stream)) != hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  return EXFOLD_OK;
+}
+
 exfold_status exfold_fold_gates(int32_t phase, int64_t T, int64_t N, int64_t K, int64_t budget,
                                 const int32_t *topk_ids, const float *topk_w,
                                 const uint8_t *keep, const int32_t *pool,
@@ -384,8 +399,11 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
   ForwardPlan p;
   exfold_status st = plan_forward(layer, T, phase, budget, p);
   if (st != EXFOLD_OK) return st;
-  if (phase != EXFOLD_PHASE_DENSE && (!tables || !tables->S || !tables->L || !tables->h))
+  if (phase == EXFOLD_PHASE_DECODE_STATIC) {
+    if (!tables || !tables->tgt || !tables->scl) return EXFOLD_ERR_NULL;
+  } else if (phase != EXFOLD_PHASE_DENSE && (!tables || !tables->S || !tables->L || !tables->h)) {
     return EXFOLD_ERR_NULL;
+  }
   if (T == 0) return EXFOLD_OK;
   if (!x || !y) return EXFOLD_ERR_NULL;
   st = check_ws(ws, ws_bytes, p.total);
@@ -421,6 +439,7 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
     e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.k_out, tables->h, tables->S,
                             tables->L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s);
   } else {
+    const bool stat = phase == EXFOLD_PHASE_DECODE_STATIC;
     e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,
                             topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s);
     if (e == hipSuccess && (int64_t)p.T * p.K <= kDecodeFrontMaxSlots) {
@@ -428,8 +447,12 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
       const PermBuffers pb = perm_buffers(p.ex, ws, dbg.offsets, dbg.row_slot);
       e = launch_decode_front(topk_ids, topk_w, p.T, p.N, p.K, p.dcap, tables->h, tables->S, tables->L,
                               pool, pool_size, fold_ids, fold_w, dbg.tgt_ids, dbg.tgt_scale,
-                              p.ex.t_shared, p.ex.gu.bm, p.ex.dn.bm, pb, s);
+                              p.ex.t_shared, p.ex.gu.bm, p.ex.dn.bm, pb, stat ? tables->tgt : nullptr,
+                              stat ? tables->scl : nullptr, s);
       permuted = true;
+    } else if (e == hipSuccess && stat) {
+      e = launch_static_remap(topk_ids, topk_w, p.T * p.K, p.N, tables->tgt, tables->scl, fold_ids,
+                              fold_w, s);
     } else if (e == hipSuccess) {
       e = launch_decode_pool_fold(topk_ids, topk_w, p.T, p.N, p.K, p.dcap, tables->h, tables->S,
                                   tables->L, true, pool, pool_size, fold_ids, fold_w, dbg.tgt_ids,

@@ -98,12 +98,16 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
   const bf16_t *Wg = (t.g < p.n_experts) ? p.W + (long long)t.g * p.w_stride : p.Ws;
 
   // global source of this thread's 16-byte chunks (row r = c / 8, chunk q = c % 8)
+  // A rows past the group's end are not loaded (their outputs are never stored):
+  // a tile with few rows (decode) then reads only its live rows.
   const bf16_t *a_src[PA];
   const bf16_t *b_src[PB];
+  bool a_live[PA];
 #pragma unroll
   for (int i = 0; i < PA; ++i) {
     const int c = i * 256 + tid;
     const int r = c >> 3;
+    a_live[i] = r < valid;
     const int rr = row0 + (r < valid ? r : 0);
     const long long arow = GATE_UP ? (long long)p.row_token[rr] : (long long)rr;
     a_src[i] = p.A + arow * p.lda + t.ks * p.kc + (c & 7) * 8;
@@ -139,7 +143,7 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
   // (macros, not lambdas taking their address), so they stay in VGPRs.
 #define EXF_GLOAD(RA, RB, K0)                                                                \
   do {                                                                                       \
-    _Pragma("unroll") for (int i_ = 0; i_ < PA; ++i_) RA[i_] =                               \
+    _Pragma("unroll") for (int i_ = 0; i_ < PA; ++i_) if (a_live[i_]) RA[i_] =               \
         *reinterpret_cast<const u32x4 *>(a_src[i_] + (K0));                                  \
     _Pragma("unroll") for (int i_ = 0; i_ < PB; ++i_) RB[i_] =                               \
         *reinterpret_cast<const u32x4 *>(b_src[i_] + (K0));                                  \
@@ -213,6 +217,7 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
     // LDS buffer (kt & 1) holds tile kt; the other register set holds tile kt + 1,
     // so each tile's loads are covered by two compute phases.
     u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
+    _Pragma("unroll") for (int i_ = 0; i_ < PA; ++i_) ra0[i_] = ra1[i_] = u32x4{0u, 0u, 0u, 0u};
     EXF_GLOAD(ra0, rb0, 0);
     EXF_LSTORE(ra0, rb0, 0);
     EXF_GLOAD(ra1, rb1, min(kBK, k_last));
@@ -234,6 +239,7 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
   } else {
     // One tile of loads in flight, covered by one compute phase.
     u32x4 ra[PA], rb[PB];
+    _Pragma("unroll") for (int i_ = 0; i_ < PA; ++i_) ra[i_] = u32x4{0u, 0u, 0u, 0u};
     EXF_GLOAD(ra, rb, 0);
     EXF_LSTORE(ra, rb, 0);
     __syncthreads();

@@ -420,6 +420,139 @@ __global__ __launch_bounds__(kPoolThreads) void decode_pool_fold_kernel(
   }
 }
 
+// Per-source tables of a decode pool (Eq. minimum_loss_assignment over the
+// pool): a source in the pool maps to itself with scale 1, any other source to
+// the first minimum of L[s, t] over the pool in pool order, with scale S[s, t].
+// Wave w takes sources w + 16 u; lane l reads L[s, pool[l + 64 c]] and
+// S[s, pool[l + 64 c]] (eight sources per batch, so 16 loads are in flight)
+// and the wave keeps the first minimum (64-bit key: value, index) with its
+// scale.  pool/in_pool/n_pool in LDS; writes tgt/scl (LDS) and tgt_g/scl_g.
+__device__ void pool_tables(int N, const float *__restrict__ S, const float *__restrict__ L,
+                            const int *pool, const int *in_pool, int n_pool, int *tgt, float *scl,
+                            int32_t *__restrict__ tgt_g, float *__restrict__ scl_g) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  constexpr int kWaves = kPoolThreads / kWave;
+  for (int base = wave; base < N; base += kWaves * 8) {
+    uint64_t best[8];
+    float bs[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      best[u] = ~0ull;
+      bs[u] = 1.0f;
+    }
+    for (int c = 0; c < n_pool; c += kWave) {
+      const int j = c + lane;
+      const bool live = j < n_pool;
+      const int pj = live ? pool[j] : 0;
+      float lv[8], sv[8];
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const size_t o = (size_t)min(base + kWaves * u, N - 1) * N + pj;
+        lv[u] = L[o];
+        sv[u] = S[o];
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const uint64_t key = live ? ((uint64_t(float_key(lv[u])) << 32) | uint64_t(j)) : ~0ull;
+        if (key < best[u]) {
+          best[u] = key;
+          bs[u] = sv[u];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int src = base + kWaves * u;
+      uint64_t b = best[u];
+#pragma unroll
+      for (int m = 32; m >= 1; m >>= 1) {
+        const uint64_t o = shfl_xor_u64(b, m);
+        b = o < b ? o : b;
+      }
+      // the lane holding the minimum (keys are distinct: they carry the index)
+      const uint64_t holder = __ballot(best[u] == b);
+      const float s_min = __shfl(bs[u], holder ? (int)__ffsll((long long)holder) - 1 : 0, kWave);
+      if (src < N && lane == 0) {
+        int t_best = src;
+        float s_best = 1.0f;
+        if (!in_pool[src] && n_pool > 0) {
+          t_best = pool[(int)(b & 0xffffffffu)];
+          s_best = s_min;
+        }
+        tgt[src] = t_best;
+        scl[src] = s_best;
+        if (tgt_g) tgt_g[src] = t_best;
+        if (scl_g) scl_g[src] = s_best;
+      }
+    }
+  }
+}
+
+// Static decode pool (Appendix B, Eq. appendix_decode_static_budget): the D
+// experts of largest h (ties to the lower id) and its per-source tables, formed
+// once; a decode step then only gathers (Eq. appendix_decode_remap).
+__global__ __launch_bounds__(kPoolThreads) void static_pool_kernel(
+    const float *__restrict__ h, int N, int D, const float *__restrict__ S,
+    const float *__restrict__ L, int32_t *__restrict__ pool_g, int32_t *__restrict__ pool_size_g,
+    int32_t *__restrict__ tgt_g, float *__restrict__ scl_g) {
+  __shared__ float hv[kMaxExperts];
+  __shared__ int pool[kMaxExperts];
+  __shared__ int in_pool[kMaxExperts];
+  __shared__ int tgt[kMaxExperts];
+  __shared__ float scl[kMaxExperts];
+  const int tid = threadIdx.x;
+  const int dcap = min(D, N);
+  if (tid < N) {
+    hv[tid] = h[tid];
+    in_pool[tid] = 0;
+  }
+  __syncthreads();
+  if (tid < N) {
+    const float v = hv[tid];
+    int rank = 0;
+    for (int e = 0; e < N; ++e) rank += (hv[e] > v) || (hv[e] == v && e < tid);
+    if (rank < dcap) {
+      pool[rank] = tid;
+      in_pool[tid] = 1;
+    }
+  }
+  __syncthreads();
+  if (tid < dcap) pool_g[tid] = pool[tid];
+  if (tid == 0) *pool_size_g = dcap;
+  pool_tables(N, S, L, pool, in_pool, dcap, tgt, scl, tgt_g, scl_g);
+}
+
+// Per-slot remap with precomputed static tables (Eq. appendix_decode_remap):
+// the grid-wide form for batches beyond the one-workgroup front end.
+__global__ __launch_bounds__(256) void static_remap_kernel(const int32_t *__restrict__ ids,
+                                                           const float *__restrict__ w, int slots,
+                                                           int N, const int32_t *__restrict__ tgt,
+                                                           const float *__restrict__ scl,
+                                                           int32_t *__restrict__ out_ids,
+                                                           float *__restrict__ out_w) {
+  const int j = blockIdx.x * 256 + threadIdx.x;
+  if (j >= slots) return;
+  const int e = clamp_id(ids[j], N);
+  const int te = clamp_id(tgt[e], N);
+  out_ids[j] = te;
+  out_w[j] = (te == e) ? w[j] : w[j] * scl[e];
+}
+
+hipError_t launch_static_remap(const int32_t *ids, const float *w, int slots, int N,
+                               const int32_t *tgt, const float *scl, int32_t *out_ids, float *out_w,
+                               hipStream_t s) {
+  if (slots <= 0) return hipSuccess;
+  static_remap_kernel<<<(slots + 255) / 256, 256, 0, s>>>(ids, w, slots, N, tgt, scl, out_ids, out_w);
+  return hipGetLastError();
+}
+
+hipError_t launch_static_pool(const float *h, int N, int D, const float *S, const float *L,
+                              int32_t *pool, int32_t *pool_size, int32_t *tgt, float *scl,
+                              hipStream_t s) {
+  static_pool_kernel<<<1, kPoolThreads, 0, s>>>(h, N, D, S, L, pool, pool_size, tgt, scl);
+  return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // Decode front end in one workgroup, after the per-token Top-K: the batch pool,
 // the per-source tables, the remap of every slot and the stable permutation of
@@ -436,7 +569,8 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     float *__restrict__ out_w, int32_t *__restrict__ tgt_g, float *__restrict__ scl_g, int t_shared,
     int bm0, int bm1, int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start0,
     int32_t *__restrict__ tile_start1, int32_t *__restrict__ row_token,
-    int32_t *__restrict__ row_slot, float *__restrict__ row_w, int32_t *__restrict__ slot_row) {
+    int32_t *__restrict__ row_slot, float *__restrict__ row_w, int32_t *__restrict__ slot_row,
+    const int32_t *__restrict__ static_tgt, const float *__restrict__ static_scl) {
   __shared__ uint8_t sid[kDecodeFrontMaxSlots];   // expert of each slot (N <= 256)
   __shared__ float sw[kDecodeFrontMaxSlots];      // its weight
   __shared__ unsigned long long wsum[kMaxExperts];
@@ -456,13 +590,21 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   const int dcap = min(D, N);
   const int groups = N + (t_shared > 0 ? 1 : 0);
 
-  const float h_e = (tid < N) ? h[tid] : 0.f;
+  const float h_e = (tid < N && h) ? h[tid] : 0.f;
+  const bool dynamic = static_tgt == nullptr;  // uniform over the workgroup
   if (tid < N) {
     wsum[tid] = 0ull;
     cnt[tid] = 0;
     in_pool[tid] = 0;
     rows_of[tid] = 0;
     rank_sh[tid] = 0;
+    if (!dynamic) {
+      // precomputed static tables: a source is in the pool iff it maps to itself
+      const int te = clamp_id(static_tgt[tid], N);
+      tgt[tid] = te;
+      scl[tid] = static_scl[tid];
+      in_pool[tid] = te == tid;
+    }
   }
   __syncthreads();
 
@@ -472,11 +614,14 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     const float wv = w[j];
     sid[j] = (uint8_t)e;
     sw[j] = wv;
-    const long long q = __double2ll_rn((double)wv * 1099511627776.0);  // 2^40
-    atomicAdd(&wsum[e], (unsigned long long)q);
-    atomicAdd(&cnt[e], 1);
+    if (dynamic) {
+      const long long q = __double2ll_rn((double)wv * 1099511627776.0);  // 2^40
+      atomicAdd(&wsum[e], (unsigned long long)q);
+      atomicAdd(&cnt[e], 1);
+    }
   }
   __syncthreads();
+  if (dynamic) {
   if (tid < N) score[tid] = (double)(long long)wsum[tid] * (double)h_e;
   const int n_cand = __syncthreads_count(tid < N && cnt[tid] > 0);
   // rank of each candidate by (score desc, id asc): thread (e, part) compares e
@@ -506,64 +651,8 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   if (tid == 0) *pool_size_g = n_pool;
 
   // ---- per-source tables (Eq. minimum_loss_assignment over the pool) ----
-  // Wave w takes sources w + 16 u; lane l reads L[s, pool[l + 64 c]] and
-  // S[s, pool[l + 64 c]] (eight sources per batch, so 16 loads are in flight)
-  // and the wave keeps the first minimum in pool order (64-bit key: value,
-  // index) together with its scale.
-  for (int base = wave; base < N; base += kFrontWaves * 8) {
-    uint64_t best[8];
-    float bs[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      best[u] = ~0ull;
-      bs[u] = 1.0f;
-    }
-    for (int c = 0; c < n_pool; c += kWave) {
-      const int j = c + lane;
-      const bool live = j < n_pool;
-      const int pj = live ? pool[j] : 0;
-      float lv[8], sv[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const size_t o = (size_t)min(base + kFrontWaves * u, N - 1) * N + pj;
-        lv[u] = L[o];
-        sv[u] = S[o];
-      }
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const uint64_t key = live ? ((uint64_t(float_key(lv[u])) << 32) | uint64_t(j)) : ~0ull;
-        if (key < best[u]) {
-          best[u] = key;
-          bs[u] = sv[u];
-        }
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int src = base + kFrontWaves * u;
-      uint64_t b = best[u];
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const uint64_t o = shfl_xor_u64(b, m);
-        b = o < b ? o : b;
-      }
-      // the lane holding the minimum (keys are distinct: they carry the index)
-      const uint64_t holder = __ballot(best[u] == b);
-      const float s_min = __shfl(bs[u], holder ? (int)__ffsll((long long)holder) - 1 : 0, kWave);
-      if (src < N && lane == 0) {
-        int t_best = src;
-        float s_best = 1.0f;
-        if (!in_pool[src] && n_pool > 0) {
-          t_best = pool[(int)(b & 0xffffffffu)];
-          s_best = s_min;
-        }
-        tgt[src] = t_best;
-        scl[src] = s_best;
-        if (tgt_g) tgt_g[src] = t_best;
-        if (scl_g) scl_g[src] = s_best;
-      }
-    }
-  }
+  pool_tables(N, S, L, pool, in_pool, n_pool, tgt, scl, tgt_g, scl_g);
+  }  // dynamic
   __syncthreads();
 
   // ---- remap every slot (Eq. decode_remap); retained slots copied ----
@@ -678,11 +767,12 @@ hipError_t launch_decode_front(const int32_t *ids, const float *w, int B, int N,
                                const float *h, const float *S, const float *L, int32_t *pool,
                                int32_t *pool_size, int32_t *out_ids, float *out_w, int32_t *tgt,
                                float *scl, int t_shared, int bm0, int bm1, const PermBuffers &pb,
-                               hipStream_t s) {
+                               const int32_t *static_tgt, const float *static_scl, hipStream_t s) {
   decode_front_kernel<<<1, kPoolThreads, 0, s>>>(ids, w, B, N, K, D, h, S, L, pool, pool_size, out_ids,
                                                  out_w, tgt, scl, t_shared, bm0, bm1, pb.offsets,
                                                  pb.tile_start0, pb.tile_start1, pb.row_token,
-                                                 pb.row_slot, pb.row_w, pb.slot_row);
+                                                 pb.row_slot, pb.row_w, pb.slot_row, static_tgt,
+                                                 static_scl);
   return hipGetLastError();
 }
 

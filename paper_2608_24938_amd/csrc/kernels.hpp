@@ -44,13 +44,23 @@ hipError_t launch_permute(const int32_t *route_ids, const float *route_w, int T,
                           int t_shared, int bm0, int bm1, const PermBuffers &pb, hipStream_t s);
 // Decode front end in one workgroup, after Top-K: pool, tables, remap and the
 // permutation of the remapped [B, K] slots (pb.blk_counts unused).  For
-// B * K <= kDecodeFrontMaxSlots.
+// B * K <= kDecodeFrontMaxSlots.  With static_tgt/static_scl (precomputed
+// tables of a static pool) the pool and table steps are skipped; h, S, L,
+// pool, pool_size, tgt and scl are then unused.
 constexpr int kDecodeFrontMaxSlots = 8192;
 hipError_t launch_decode_front(const int32_t *ids, const float *w, int B, int N, int K, int D,
                                const float *h, const float *S, const float *L, int32_t *pool,
                                int32_t *pool_size, int32_t *out_ids, float *out_w, int32_t *tgt,
                                float *scl, int t_shared, int bm0, int bm1, const PermBuffers &pb,
+                               const int32_t *static_tgt, const float *static_scl, hipStream_t s);
+// Per-slot remap of [slots] routes with static tables (grid-wide).
+hipError_t launch_static_remap(const int32_t *ids, const float *w, int slots, int N,
+                               const int32_t *tgt, const float *scl, int32_t *out_ids, float *out_w,
                                hipStream_t s);
+// Static decode pool TopK(h, D) and its per-source tables (one workgroup).
+hipError_t launch_static_pool(const float *h, int N, int D, const float *S, const float *L,
+                              int32_t *pool, int32_t *pool_size, int32_t *tgt, float *scl,
+                              hipStream_t s);
 
 // ---- expert GEMMs and combine (k_gemm.hip) ----
 enum { kGemmSimt = 0, kGemmTile = 1 };

@@ -19,11 +19,11 @@ _lib = None
 
 OK, ERR_NULL, ERR_SHAPE, ERR_BUDGET, ERR_DTYPE, ERR_WORKSPACE, ERR_DEVICE, ERR_UNSUPPORTED, ERR_ARG = range(9)
 F32, BF16 = 0, 1
-PHASE = {"dense": 0, "prefill": 1, "decode": 2}
+PHASE = {"dense": 0, "prefill": 1, "decode": 2, "decode_static": 3}
 CAL_MODE = {"corouted": 0, "common": 1}
 
 EXPORTED = [
-    "exfold_select_prefill", "exfold_select_decode_pool", "exfold_fold_gates",
+    "exfold_select_prefill", "exfold_select_decode_pool", "exfold_fold_gates", "exfold_static_pool",
     "exfold_moe_workspace_size", "exfold_moe_forward", "exfold_execute_workspace_size",
     "exfold_moe_execute", "exfold_calibrate_workspace_size", "exfold_calibrate_projectors",
     "exfold_status_str",
@@ -45,7 +45,8 @@ class _Layer(ctypes.Structure):
 
 
 class _Tables(ctypes.Structure):
-    _fields_ = [("S", ctypes.c_void_p), ("L", ctypes.c_void_p), ("h", ctypes.c_void_p)]
+    _fields_ = [("S", ctypes.c_void_p), ("L", ctypes.c_void_p), ("h", ctypes.c_void_p),
+                ("tgt", ctypes.c_void_p), ("scl", ctypes.c_void_p)]
 
 
 _DEBUG_FIELDS = ["logits", "topk_ids", "topk_w", "keep", "pool", "pool_size", "tgt_ids", "tgt_scale",
@@ -73,6 +74,7 @@ def lib() -> ctypes.CDLL:
             "exfold_select_prefill": (i32, [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp]),
             "exfold_select_decode_pool": (i32, [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp]),
             "exfold_fold_gates": (i32, [i32, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "exfold_static_pool": (i32, [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp]),
             "exfold_moe_workspace_size": (sz, [vp, i64, i32, i64]),
             "exfold_moe_forward": (i32, [vp, vp, vp, i64, i32, i64, vp, vp, vp, sz, vp]),
             "exfold_execute_workspace_size": (sz, [vp, i64, i64]),
@@ -207,6 +209,19 @@ def fold_gates(phase, budget, topk_ids, topk_w, S, L, keep=None, pool=None, pool
     return (out_ids, out_w, tgt, scl) if tables else (out_ids, out_w)
 
 
+def static_pool(h, budget, S, L, stream=None):
+    """Static decode pool TopK(h, D) and its per-source tables. Returns (pool, pool_size, tgt, scl)."""
+    N = h.shape[0]
+    dev = h.device
+    pool = torch.empty((min(budget, N),), dtype=torch.int32, device=dev)
+    pool_size = torch.empty((1,), dtype=torch.int32, device=dev)
+    tgt = torch.empty((N,), dtype=torch.int32, device=dev)
+    scl = torch.empty((N,), dtype=torch.float32, device=dev)
+    _check(lib().exfold_static_pool(_ptr(h), N, budget, _ptr(S), _ptr(L), _ptr(pool), _ptr(pool_size), _ptr(tgt),
+                                    _ptr(scl), _stream(stream)), "exfold_static_pool")
+    return pool, pool_size, tgt, scl
+
+
 def moe_workspace_size(layer: Layer, T: int, phase: str, budget: int) -> int:
     ls = layer.struct()
     n = lib().exfold_moe_workspace_size(ctypes.byref(ls), T, PHASE[phase], budget)
@@ -238,16 +253,18 @@ def debug_buffers(layer: Layer, T: int, phase: str, budget: int, device) -> dict
 
 
 def moe_forward(layer: Layer, x, phase: str = "dense", budget: int = 0, S=None, L=None, h=None, y=None,
-                debug: dict | None = None, workspace=None, stream=None, events=None):
+                debug: dict | None = None, workspace=None, stream=None, events=None, static_tables=None):
     """Folded MoE layer forward; returns y [T, d] (dtype of the layer).
 
+    static_tables: (tgt, scl) from static_pool, for phase "decode_static".
     events: optional ctypes array of N_EVENTS hipEvent_t handles recorded at the stage boundaries."""
     T = x.shape[0]
     _need(x, layer.dtype, (T, layer.d), "x")
     if y is None:
         y = torch.empty_like(x)
     ls = layer.struct()
-    tb = _Tables(_ptr(S), _ptr(L), _ptr(h)) if S is not None else None
+    tgt, scl = static_tables if static_tables is not None else (None, None)
+    tb = _Tables(_ptr(S), _ptr(L), _ptr(h), _ptr(tgt), _ptr(scl)) if (S is not None or tgt is not None) else None
     dbg = None
     if debug is not None or events is not None:
         debug = debug or {}

@@ -51,8 +51,9 @@ def ws_size(ly, T=64, phase=1, budget=1):
     return X.lib().exfold_moe_workspace_size(ctypes.byref(ly), T, phase, budget)
 
 
-def forward(ly, T=64, phase=1, budget=1, tables=True, ws_bytes=None, x=FAKE, y=FAKE, ws=FAKE * 16):
-    tb = X._Tables(FAKE, FAKE, FAKE)
+def forward(ly, T=64, phase=1, budget=1, tables=True, ws_bytes=None, x=FAKE, y=FAKE, ws=FAKE * 16,
+            static=(FAKE, FAKE)):
+    tb = X._Tables(FAKE, FAKE, FAKE, *static)
     if ws_bytes is None:
         ws_bytes = 0
     return X.lib().exfold_moe_forward(ctypes.byref(ly), ctypes.byref(tb) if tables else None, x, T, phase,
@@ -95,6 +96,11 @@ def test_forward_validation_codes():
     assert forward(ly, T=0) == X.OK                                           # empty batch: no-op
     # dense phase needs no tables
     assert forward(ly, phase=0, tables=False, ws_bytes=0) == X.ERR_WORKSPACE
+    # the static decode phase needs the precomputed per-source tables
+    assert forward(ly, phase=3, budget=4, static=(None, None)) == X.ERR_NULL
+    assert forward(ly, phase=3, budget=4, static=(FAKE, None)) == X.ERR_NULL
+    assert forward(ly, phase=3, budget=0) == X.ERR_BUDGET
+    assert forward(ly, phase=3, budget=4, ws_bytes=0) == X.ERR_WORKSPACE
 
 
 def test_workspace_grows_with_tokens_and_budget():
@@ -120,6 +126,12 @@ def test_select_and_fold_validation():
     assert L.exfold_fold_gates(1, 4, 8, 2, 1, f, f, None, f, f, f, f, f, f, None, None, None) == X.ERR_NULL
     assert L.exfold_fold_gates(2, 4, 8, 2, 1, f, f, None, None, f, f, f, f, f, None, None, None) == X.ERR_NULL
     assert L.exfold_fold_gates(2, 4, 8, 2, 1, f, f, None, f, f, None, f, f, f, None, None, None) == X.ERR_NULL
+    assert L.exfold_fold_gates(3, 4, 8, 2, 1, f, f, None, f, f, f, f, f, f, None, None, None) == X.ERR_ARG
+    assert L.exfold_static_pool(f, 8, 0, f, f, f, f, f, f, None) == X.ERR_BUDGET
+    assert L.exfold_static_pool(f, 0, 4, f, f, f, f, f, f, None) == X.ERR_SHAPE
+    assert L.exfold_static_pool(f, 512, 4, f, f, f, f, f, f, None) == X.ERR_UNSUPPORTED
+    assert L.exfold_static_pool(f, 8, 4, f, f, f, f, None, f, None) == X.ERR_NULL
+    assert L.exfold_static_pool(None, 8, 4, f, f, f, f, f, f, None) == X.ERR_NULL
 
 
 def test_calibrate_validation():
