@@ -78,6 +78,22 @@ enum {
   EXFOLD_CAL_COMMON = 1     /* every expert on every calibration token (common input) */
 };
 
+/* Prefill fold safeguards (bits of exfold_tables.fold_flags and of the
+ * fold_flags argument of exfold_fold_gates); 0 = the main method.
+ *   LOSS_CAP:   a pair (s, t) with L[s, t] > loss_cap is not a candidate target;
+ *               an omitted route with no candidate is dropped (Appendix C:
+ *               directed pairs with calibrated loss above 0.99 excluded).
+ *   RENORM:     after folding, the retained weights are scaled by (sum of the K
+ *               router weights) / (sum of the folded weights) when that sum is
+ *               positive (Appendix C: the routed-weight sum is preserved).
+ *   CONFIDENCE: c_s = clip(1 - min_t L[s, t], 0, 1); the target receives
+ *               w_s c_s S[s, t] and w_s (1 - c_s) is spread over the retained
+ *               routes in proportion to their router weights (Appendix F,
+ *               Eq. dsv4_confidence, with L as the source-relative residual).
+ * Safeguard arithmetic is float64, rounded once to float32 (see the oracle's
+ * fold_prefill_safeguarded for the order of operations). */
+enum { EXFOLD_FOLD_LOSS_CAP = 1, EXFOLD_FOLD_RENORM = 2, EXFOLD_FOLD_CONFIDENCE = 4 };
+
 /* One MoE layer.  Pointers are device memory of dtype `dtype` unless noted. */
 typedef struct exfold_layer {
   int64_t d;              /* hidden size                                          */
@@ -105,6 +121,8 @@ typedef struct exfold_tables {
   const float *h;      /* [N]    float32 */
   const int32_t *tgt;  /* [N]    int32: target of each source expert, or NULL */
   const float *scl;    /* [N]    float32: its scale, or NULL                  */
+  float loss_cap;      /* prefill: cap of EXFOLD_FOLD_LOSS_CAP                */
+  int32_t fold_flags;  /* prefill: EXFOLD_FOLD_* safeguards, 0 = none         */
 } exfold_tables;
 
 /* Stage boundaries at which exfold_moe_forward records the optional events. */
@@ -182,6 +200,7 @@ exfold_status exfold_select_decode_pool(const float *logits, int64_t B, int64_t 
  *            outside the pool becomes (tgt[s], w * S[s, tgt[s]]) with one float32
  *            multiply; retained slots are copied.  tgt_ids/tgt_scale [N] are
  *            optional outputs of the per-source tables (NULL to skip).
+ *   loss_cap/fold_flags: PREFILL safeguards (EXFOLD_FOLD_*); ignored in DECODE.
  *   Unused arguments of the other phase may be NULL.
  */
 exfold_status exfold_fold_gates(int32_t phase, int64_t T, int64_t N, int64_t K, int64_t budget,
@@ -189,7 +208,8 @@ exfold_status exfold_fold_gates(int32_t phase, int64_t T, int64_t N, int64_t K, 
                                 const uint8_t *keep, const int32_t *pool,
                                 const int32_t *pool_size, const float *S, const float *L,
                                 int32_t *out_ids, float *out_w, int32_t *tgt_ids,
-                                float *tgt_scale, void *stream);
+                                float *tgt_scale, float loss_cap, int32_t fold_flags,
+                                void *stream);
 
 /*
  * Static decode pool (Appendix B, Eq. appendix_decode_static_budget): formed

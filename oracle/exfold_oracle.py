@@ -64,6 +64,13 @@ READINGS = {
     "R13": "Decode keeps the [B,K] layout; duplicate ids after remapping are executed twice.",
     "R14": "Decode remapped weight: one float32 multiply w*S (retained slots copied).",
     "R15": "Shared expert: weight 1, added to every token, never selected or folded.",
+    "R22": "Loss-cap safeguard: pairs with L > cap are not candidate targets; an omitted "
+           "route without a candidate is dropped.",
+    "R23": "Confidence split: c_s = clip(1 - min L[s, t], 0, 1) with L as the source-relative "
+           "residual; the remainder w_s (1 - c_s) goes to the retained routes in proportion "
+           "to their router weights.",
+    "R24": "Renormalisation: retained weights scaled by (sum of the K router weights) / "
+           "(sum of the folded weights) when that sum is positive.",
 }
 
 FIXED_POINT_BITS = 40       # R6
@@ -256,6 +263,80 @@ def fold_prefill(ids, w, keep, S, L):
         for c, j in enumerate(ret):
             out_ids[i, c] = ids[i, j]
             out_w[i, c] = np.float32(acc[j])
+    return out_ids, out_w
+
+
+def fold_prefill_safeguarded(ids, w, keep, S, L, loss_cap=None, renorm: bool = False,
+                             confidence: bool = False):
+    """Prefill fold with the safeguards of the cross-model and DeepSeek-V4
+    configurations (Appendix C; Appendix F, Eq. dsv4_confidence).
+
+    * loss_cap: a directed pair (s, t) with L[s, t] > loss_cap is not a
+      candidate target; an omitted route with no candidate is dropped (R22).
+    * confidence: c_s = clip(1 - min over candidates of L[s, t], 0, 1); the
+      minimum-loss target t* receives w_s c_s S[s, t*] and the remainder
+      w_s (1 - c_s) is spread over the retained routes in proportion to their
+      router weights, w_t / sum of retained w (R23; L is the source-relative
+      residual of Eq. dsv4_confidence).
+    * renorm: after folding, the retained weights are scaled by
+      (sum of all K router weights) / (sum of the folded weights), when that
+      sum is positive (R24).
+
+    Arithmetic is float64 in this order, every product and sum rounded once
+    (no fused multiply-add): for each retained route t (route order),
+    acc_t = w_t, then for each omitted route s (route order) acc_t += (w_s c_s)
+    S[s, t] if t is its target, then acc_t += (w_s (1 - c_s)) (w_t / W_ret);
+    finally acc_t * (W_all / sum acc) when renormalising; one rounding to float32.
+    Without safeguards the result equals ``fold_prefill``.
+    """
+    ids = np.asarray(ids)
+    t, k = ids.shape
+    k_out = int(np.asarray(keep)[0].sum()) if t else 0
+    out_ids = np.zeros((t, k_out), dtype=np.int32)
+    out_w = np.zeros((t, k_out), dtype=np.float32)
+    S = np.asarray(S, dtype=np.float32)
+    L = np.asarray(L, dtype=np.float32)
+    ww = _f64(w)
+    for i in range(t):
+        ret = [j for j in range(k) if keep[i, j]]
+        assert len(ret) == k_out
+        acc = {j: ww[i, j] for j in ret}
+        w_ret = 0.0
+        for j in ret:
+            w_ret += ww[i, j]
+        for j in range(k):
+            if keep[i, j]:
+                continue
+            s = int(ids[i, j])
+            cands = [q for q in ret if loss_cap is None or float(L[s, ids[i, q]]) <= loss_cap]
+            if not cands:
+                continue                                    # no admissible target: dropped
+            q_t = cands[0]
+            for q in cands[1:]:                             # first minimum in route order
+                if L[s, ids[i, q]] < L[s, ids[i, q_t]]:
+                    q_t = q
+            c = 1.0
+            if confidence:
+                c = min(1.0, max(0.0, 1.0 - float(L[s, ids[i, q_t]])))
+            acc[q_t] = acc[q_t] + (ww[i, j] * c) * float(S[s, ids[i, q_t]])
+            if confidence:
+                rest = ww[i, j] * (1.0 - c)
+                for q in ret:
+                    acc[q] = acc[q] + rest * (ww[i, q] / w_ret)
+        if renorm:
+            w_all = 0.0
+            for j in range(k):
+                w_all += ww[i, j]
+            tot = 0.0
+            for j in ret:
+                tot += acc[j]
+            if tot > 0.0:
+                f = w_all / tot
+                for j in ret:
+                    acc[j] = acc[j] * f
+        for c_, j in enumerate(ret):
+            out_ids[i, c_] = ids[i, j]
+            out_w[i, c_] = np.float32(acc[j])
     return out_ids, out_w
 
 

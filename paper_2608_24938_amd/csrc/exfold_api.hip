@@ -271,6 +271,13 @@ exfold_status plan_calibrate(const exfold_layer *L, int64_t m, int32_t mode, Cal
   return EXFOLD_OK;
 }
 
+bool valid_fold_opts(float loss_cap, int32_t flags) {
+  constexpr int32_t kAll = EXFOLD_FOLD_LOSS_CAP | EXFOLD_FOLD_RENORM | EXFOLD_FOLD_CONFIDENCE;
+  if (flags & ~kAll) return false;
+  if ((flags & EXFOLD_FOLD_LOSS_CAP) && !(loss_cap == loss_cap)) return false;  // NaN cap
+  return true;
+}
+
 exfold_status check_ws(void *ws, size_t ws_bytes, size_t need) {
   if (need > 0 && !ws) return EXFOLD_ERR_NULL;
   if (ws_bytes < need) return EXFOLD_ERR_WORKSPACE;
@@ -356,7 +363,9 @@ exfold_status exfold_fold_gates(int32_t phase, int64_t T, int64_t N, int64_t K, 
                                 const uint8_t *keep, const int32_t *pool,
                                 const int32_t *pool_size, const float *S, const float *L,
                                 int32_t *out_ids, float *out_w, int32_t *tgt_ids,
-                                float *tgt_scale, void *stream) {
+                                float *tgt_scale, float loss_cap, int32_t fold_flags,
+                                void *stream) {
+  if (!valid_fold_opts(loss_cap, fold_flags)) return EXFOLD_ERR_ARG;
   if (phase != EXFOLD_PHASE_PREFILL && phase != EXFOLD_PHASE_DECODE) return EXFOLD_ERR_ARG;
   exfold_status st = check_routing(T, N, K);
   if (st != EXFOLD_OK) return st;
@@ -369,7 +378,7 @@ exfold_status exfold_fold_gates(int32_t phase, int64_t T, int64_t N, int64_t K, 
     const int kp = (int)(budget > K ? K : budget);
     if (launch_route_tokens(nullptr, 0, nullptr, nullptr, (int)T, (int)N, (int)K, kp, nullptr, S, L,
                             const_cast<int32_t *>(topk_ids), const_cast<float *>(topk_w), nullptr,
-                            keep, out_ids, out_w, s) != hipSuccess)
+                            keep, out_ids, out_w, s, loss_cap, fold_flags) != hipSuccess)
       return EXFOLD_ERR_DEVICE;
     return EXFOLD_OK;
   }
@@ -404,6 +413,8 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
   } else if (phase != EXFOLD_PHASE_DENSE && (!tables || !tables->S || !tables->L || !tables->h)) {
     return EXFOLD_ERR_NULL;
   }
+  if (phase == EXFOLD_PHASE_PREFILL && !valid_fold_opts(tables->loss_cap, tables->fold_flags))
+    return EXFOLD_ERR_ARG;
   if (T == 0) return EXFOLD_OK;
   if (!x || !y) return EXFOLD_ERR_NULL;
   st = check_ws(ws, ws_bytes, p.total);
@@ -437,7 +448,8 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
     exec_w = topk_w;
   } else if (phase == EXFOLD_PHASE_PREFILL) {
     e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.k_out, tables->h, tables->S,
-                            tables->L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s);
+                            tables->L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s,
+                            tables->loss_cap, tables->fold_flags);
   } else {
     const bool stat = phase == EXFOLD_PHASE_DECODE_STATIC;
     e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,

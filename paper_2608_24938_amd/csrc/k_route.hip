@@ -226,7 +226,7 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
     float *__restrict__ logits_out, int T, int N, int K, int k_pre, const float *__restrict__ h,
     const float *__restrict__ S, const float *__restrict__ L, int32_t *__restrict__ topk_ids,
     float *__restrict__ topk_w, uint8_t *__restrict__ keep, const uint8_t *__restrict__ keep_in,
-    int32_t *__restrict__ fold_ids, float *__restrict__ fold_w) {
+    int32_t *__restrict__ fold_ids, float *__restrict__ fold_w, float loss_cap, int flags) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // uniform per wave
@@ -268,9 +268,13 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
 #pragma unroll
   for (int j = 0; j < kMaxTopK; ++j) ids[j] = __shfl(my_id, j < K ? j : 0, kWave);
 
-  // Omitted route: first minimum of L[s, t] over the retained routes in route order.
+  // Omitted route: first minimum of L[s, t] over the retained routes in route
+  // order (with the loss cap: over those with L[s, t] <= cap; none -> dropped).
+  // Safeguard arithmetic is float64 with explicit roundings (no fused
+  // multiply-add), in the order the fold is defined in.
+  const bool capped = flags & EXFOLD_FOLD_LOSS_CAP, conf = flags & EXFOLD_FOLD_CONFIDENCE;
   int tgt_lane = -1;
-  double contrib = 0.0;
+  double contrib = 0.0, rest = 0.0;
   if (lane < K && !kept) {
     const float *lrow = L + (size_t)my_id * N;
     float lv[kMaxTopK];
@@ -279,21 +283,44 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
     float best = 0.f;
 #pragma unroll
     for (int j = 0; j < kMaxTopK; ++j) {
-      if (j < K && ((kmask >> j) & 1ull)) {
+      if (j < K && ((kmask >> j) & 1ull) && (!capped || lv[j] <= loss_cap)) {
         if (tgt_lane < 0 || lv[j] < best) {
           best = lv[j];
           tgt_lane = j;
         }
       }
     }
-    if (tgt_lane >= 0) contrib = (double)my_w * (double)S[(size_t)my_id * N + ids[tgt_lane]];
+    if (tgt_lane >= 0) {
+      double c = 1.0;
+      if (conf) c = fmin(1.0, fmax(0.0, __dsub_rn(1.0, (double)best)));
+      contrib = __dmul_rn(__dmul_rn((double)my_w, c), (double)S[(size_t)my_id * N + ids[tgt_lane]]);
+      if (conf) rest = __dmul_rn((double)my_w, __dsub_rn(1.0, c));
+    }
   }
-  // Coalesce onto each retained route, omitted routes in route order.
+  // Coalesce onto each retained route, omitted routes in route order: the
+  // target's share, then (confidence split) the spread w_s (1 - c_s) w_t / W_ret.
+  double w_ret = 0.0;
+  if (conf)
+    for (int j = 0; j < K; ++j)
+      if ((kmask >> j) & 1ull) w_ret = __dadd_rn(w_ret, (double)__shfl(my_w, j, kWave));
+  const double share = (conf && kept) ? __ddiv_rn((double)my_w, w_ret) : 0.0;
   double acc = (double)my_w;
   for (int j = 0; j < K; ++j) {
     const int tl = __shfl(tgt_lane, j, kWave);
     const double c = shfl_f64(contrib, j);
-    if (tl == lane) acc += c;
+    const double r = shfl_f64(rest, j);
+    if (tl == lane) acc = __dadd_rn(acc, c);
+    if (conf && tl >= 0 && kept) acc = __dadd_rn(acc, __dmul_rn(r, share));
+  }
+  // Renormalisation: scale the retained weights to the sum of the K router weights.
+  if (flags & EXFOLD_FOLD_RENORM) {
+    double w_all = 0.0, tot = 0.0;
+    for (int j = 0; j < K; ++j) {
+      w_all = __dadd_rn(w_all, (double)__shfl(my_w, j, kWave));
+      const double a = shfl_f64(acc, j);
+      if ((kmask >> j) & 1ull) tot = __dadd_rn(tot, a);
+    }
+    if (tot > 0.0) acc = __dmul_rn(acc, __ddiv_rn(w_all, tot));
   }
   // Retained routes in route order; a caller-supplied keep row with more than
   // k_out ones has its extra routes dropped (never written out of bounds).
@@ -309,10 +336,11 @@ hipError_t launch_route_tokens(const float *part, int P, const float *bias, floa
                                int N, int K, int k_pre, const float *h, const float *S, const float *L,
                                int32_t *topk_ids, float *topk_w, uint8_t *keep,
                                const uint8_t *keep_in, int32_t *fold_ids, float *fold_w,
-                               hipStream_t s) {
+                               hipStream_t s, float loss_cap, int flags) {
   if (T <= 0) return hipSuccess;
   route_tokens_kernel<<<(T + 3) / 4, 256, 0, s>>>(part, P, bias, logits_out, T, N, K, k_pre, h, S, L,
-                                                  topk_ids, topk_w, keep, keep_in, fold_ids, fold_w);
+                                                  topk_ids, topk_w, keep, keep_in, fold_ids, fold_w,
+                                                  loss_cap, flags);
   return hipGetLastError();
 }
 

@@ -15,11 +15,12 @@ int router_splits(int dtype, int T, int N, int d);
 // Per-token Top-K + softmax (if part != nullptr: logits = sum of the P partials
 // + bias, written to logits_out if given), prefill selection (if keep or fold
 // outputs are requested) and prefill fold (if fold_ids != nullptr).
+// loss_cap/flags: the prefill fold safeguards (EXFOLD_FOLD_* bits).
 hipError_t launch_route_tokens(const float *part, int P, const float *bias, float *logits_out, int T,
                                int N, int K, int k_pre, const float *h, const float *S, const float *L,
                                int32_t *topk_ids, float *topk_w, uint8_t *keep,
                                const uint8_t *keep_in, int32_t *fold_ids, float *fold_w,
-                               hipStream_t s);
+                               hipStream_t s, float loss_cap = 0.f, int flags = 0);
 // Decode pool (if do_pool) and per-source tables + per-slot remap (if out_ids).
 hipError_t launch_decode_pool_fold(const int32_t *ids, const float *w, int B, int N, int K, int D,
                                    const float *h, const float *S, const float *L, bool do_pool,

@@ -46,7 +46,18 @@ class _Layer(ctypes.Structure):
 
 class _Tables(ctypes.Structure):
     _fields_ = [("S", ctypes.c_void_p), ("L", ctypes.c_void_p), ("h", ctypes.c_void_p),
-                ("tgt", ctypes.c_void_p), ("scl", ctypes.c_void_p)]
+                ("tgt", ctypes.c_void_p), ("scl", ctypes.c_void_p), ("loss_cap", ctypes.c_float),
+                ("fold_flags", ctypes.c_int32)]
+
+
+FOLD_LOSS_CAP, FOLD_RENORM, FOLD_CONFIDENCE = 1, 2, 4
+
+
+def fold_opts(loss_cap=None, renorm=False, confidence=False):
+    """(loss_cap, fold_flags) of the prefill fold safeguards (EXFOLD_FOLD_* in the header)."""
+    flags = (FOLD_LOSS_CAP if loss_cap is not None else 0) | (FOLD_RENORM if renorm else 0) | \
+        (FOLD_CONFIDENCE if confidence else 0)
+    return (0.0 if loss_cap is None else float(loss_cap)), flags
 
 
 _DEBUG_FIELDS = ["logits", "topk_ids", "topk_w", "keep", "pool", "pool_size", "tgt_ids", "tgt_scale",
@@ -73,7 +84,8 @@ def lib() -> ctypes.CDLL:
         sig = {
             "exfold_select_prefill": (i32, [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp]),
             "exfold_select_decode_pool": (i32, [vp, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp]),
-            "exfold_fold_gates": (i32, [i32, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp]),
+            "exfold_fold_gates": (i32, [i32, i64, i64, i64, i64, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp, vp,
+                                        ctypes.c_float, i32, vp]),
             "exfold_static_pool": (i32, [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp]),
             "exfold_moe_workspace_size": (sz, [vp, i64, i32, i64]),
             "exfold_moe_forward": (i32, [vp, vp, vp, i64, i32, i64, vp, vp, vp, sz, vp]),
@@ -192,8 +204,10 @@ def select_decode_pool(h, budget, logits=None, topk_ids=None, topk_w=None, top_k
 
 
 def fold_gates(phase, budget, topk_ids, topk_w, S, L, keep=None, pool=None, pool_size=None, tables=False,
-               stream=None):
-    """Fold route metadata. Returns (out_ids, out_w) or (out_ids, out_w, tgt, scl) with tables=True."""
+               stream=None, loss_cap=None, renorm=False, confidence=False):
+    """Fold route metadata. Returns (out_ids, out_w) or (out_ids, out_w, tgt, scl) with tables=True.
+
+    loss_cap/renorm/confidence: the prefill safeguards (see fold_opts)."""
     T, K = topk_ids.shape
     N = S.shape[0]
     ph = PHASE[phase]
@@ -205,7 +219,8 @@ def fold_gates(phase, budget, topk_ids, topk_w, S, L, keep=None, pool=None, pool
     scl = torch.empty((N,), dtype=torch.float32, device=dev) if tables else None
     _check(lib().exfold_fold_gates(ph, T, N, K, budget, _ptr(topk_ids), _ptr(topk_w), _ptr(keep), _ptr(pool),
                                    _ptr(pool_size), _ptr(S), _ptr(L), _ptr(out_ids), _ptr(out_w), _ptr(tgt),
-                                   _ptr(scl), _stream(stream)), "exfold_fold_gates")
+                                   _ptr(scl), *fold_opts(loss_cap, renorm, confidence), _stream(stream)),
+           "exfold_fold_gates")
     return (out_ids, out_w, tgt, scl) if tables else (out_ids, out_w)
 
 
@@ -253,10 +268,12 @@ def debug_buffers(layer: Layer, T: int, phase: str, budget: int, device) -> dict
 
 
 def moe_forward(layer: Layer, x, phase: str = "dense", budget: int = 0, S=None, L=None, h=None, y=None,
-                debug: dict | None = None, workspace=None, stream=None, events=None, static_tables=None):
+                debug: dict | None = None, workspace=None, stream=None, events=None, static_tables=None,
+                safeguards: dict | None = None):
     """Folded MoE layer forward; returns y [T, d] (dtype of the layer).
 
     static_tables: (tgt, scl) from static_pool, for phase "decode_static".
+    safeguards: prefill fold safeguards, keyword arguments of fold_opts.
     events: optional ctypes array of N_EVENTS hipEvent_t handles recorded at the stage boundaries."""
     T = x.shape[0]
     _need(x, layer.dtype, (T, layer.d), "x")
@@ -264,7 +281,9 @@ def moe_forward(layer: Layer, x, phase: str = "dense", budget: int = 0, S=None, 
         y = torch.empty_like(x)
     ls = layer.struct()
     tgt, scl = static_tables if static_tables is not None else (None, None)
-    tb = _Tables(_ptr(S), _ptr(L), _ptr(h), _ptr(tgt), _ptr(scl)) if (S is not None or tgt is not None) else None
+    cap, flags = fold_opts(**(safeguards or {}))
+    tb = _Tables(_ptr(S), _ptr(L), _ptr(h), _ptr(tgt), _ptr(scl), cap, flags) \
+        if (S is not None or tgt is not None) else None
     dbg = None
     if debug is not None or events is not None:
         debug = debug or {}

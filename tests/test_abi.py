@@ -52,8 +52,8 @@ def ws_size(ly, T=64, phase=1, budget=1):
 
 
 def forward(ly, T=64, phase=1, budget=1, tables=True, ws_bytes=None, x=FAKE, y=FAKE, ws=FAKE * 16,
-            static=(FAKE, FAKE)):
-    tb = X._Tables(FAKE, FAKE, FAKE, *static)
+            static=(FAKE, FAKE), flags=(0.0, 0)):
+    tb = X._Tables(FAKE, FAKE, FAKE, *static, *flags)
     if ws_bytes is None:
         ws_bytes = 0
     return X.lib().exfold_moe_forward(ctypes.byref(ly), ctypes.byref(tb) if tables else None, x, T, phase,
@@ -101,6 +101,10 @@ def test_forward_validation_codes():
     assert forward(ly, phase=3, budget=4, static=(FAKE, None)) == X.ERR_NULL
     assert forward(ly, phase=3, budget=0) == X.ERR_BUDGET
     assert forward(ly, phase=3, budget=4, ws_bytes=0) == X.ERR_WORKSPACE
+    # unknown safeguard bits or a NaN loss cap
+    assert forward(ly, flags=(0.0, 16)) == X.ERR_ARG
+    assert forward(ly, flags=(float("nan"), 1)) == X.ERR_ARG
+    assert forward(ly, flags=(0.99, 7), ws_bytes=0) == X.ERR_WORKSPACE
 
 
 def test_workspace_grows_with_tokens_and_budget():
@@ -121,12 +125,15 @@ def test_select_and_fold_validation():
     assert L.exfold_select_prefill(f, 0, 8, 2, 1, f, f, f, f, None) == X.OK
     assert L.exfold_select_decode_pool(f, 4, 8, 2, 0, f, f, f, f, f, None) == X.ERR_BUDGET
     assert L.exfold_select_decode_pool(f, 4, 8, 2, 3, f, f, f, None, f, None) == X.ERR_NULL
-    assert L.exfold_fold_gates(7, 4, 8, 2, 1, f, f, f, f, f, f, f, f, f, None, None, None) == X.ERR_ARG
-    assert L.exfold_fold_gates(1, 4, 8, 2, 0, f, f, f, f, f, f, f, f, f, None, None, None) == X.ERR_BUDGET
-    assert L.exfold_fold_gates(1, 4, 8, 2, 1, f, f, None, f, f, f, f, f, f, None, None, None) == X.ERR_NULL
-    assert L.exfold_fold_gates(2, 4, 8, 2, 1, f, f, None, None, f, f, f, f, f, None, None, None) == X.ERR_NULL
-    assert L.exfold_fold_gates(2, 4, 8, 2, 1, f, f, None, f, f, None, f, f, f, None, None, None) == X.ERR_NULL
-    assert L.exfold_fold_gates(3, 4, 8, 2, 1, f, f, None, f, f, f, f, f, f, None, None, None) == X.ERR_ARG
+    assert L.exfold_fold_gates(7, 4, 8, 2, 1, f, f, f, f, f, f, f, f, f, None, None, 0.0, 0, None) == X.ERR_ARG
+    assert L.exfold_fold_gates(1, 4, 8, 2, 0, f, f, f, f, f, f, f, f, f, None, None, 0.0, 0, None) == X.ERR_BUDGET
+    assert L.exfold_fold_gates(1, 4, 8, 2, 1, f, f, None, f, f, f, f, f, f, None, None, 0.0, 0, None) == X.ERR_NULL
+    assert L.exfold_fold_gates(2, 4, 8, 2, 1, f, f, None, None, f, f, f, f, f, None, None, 0.0, 0, None) == X.ERR_NULL
+    assert L.exfold_fold_gates(2, 4, 8, 2, 1, f, f, None, f, f, None, f, f, f, None, None, 0.0, 0, None) == X.ERR_NULL
+    assert L.exfold_fold_gates(3, 4, 8, 2, 1, f, f, None, f, f, f, f, f, f, None, None, 0.0, 0, None) == X.ERR_ARG
+    assert L.exfold_fold_gates(1, 4, 8, 2, 1, f, f, f, f, f, f, f, f, f, None, None, 0.5, 8, None) == X.ERR_ARG
+    assert L.exfold_fold_gates(1, 4, 8, 2, 1, f, f, f, f, f, f, f, f, f, None, None, float("nan"), 1,
+                               None) == X.ERR_ARG
     assert L.exfold_static_pool(f, 8, 0, f, f, f, f, f, f, None) == X.ERR_BUDGET
     assert L.exfold_static_pool(f, 0, 4, f, f, f, f, f, f, None) == X.ERR_SHAPE
     assert L.exfold_static_pool(f, 512, 4, f, f, f, f, f, f, None) == X.ERR_UNSUPPORTED

@@ -45,6 +45,13 @@ MUTANTS = {
     "self scalar zero": ("S[s, t], Lo[s, t] = 1.0, 0.0", "S[s, t], Lo[s, t] = 0.0, 0.0"),
     "h is max norm": ("h[observed] = norm_sum[observed] / norm_cnt[observed]", "h[observed] = norm_sum[observed]"),
     "storage counts one table": ("return n_layers * n_experts * n_experts * 4 * 2", "return n_layers * n_experts * n_experts * 4"),
+    "loss cap exclusive": ("float(L[s, ids[i, q]]) <= loss_cap]", "float(L[s, ids[i, q]]) < loss_cap]"),
+    "capped route spread instead of dropped": ("                continue                                    # no admissible target: dropped",
+                                              "                cands = ret"),
+    "confidence not clipped": ("c = min(1.0, max(0.0, 1.0 - float(L[s, ids[i, q_t]])))", "c = 1.0 - float(L[s, ids[i, q_t]])"),
+    "confidence spread uniform": ("acc[q] = acc[q] + rest * (ww[i, q] / w_ret)", "acc[q] = acc[q] + rest / len(ret)"),
+    "confidence remainder to target": ("acc[q] = acc[q] + rest * (ww[i, q] / w_ret)", "acc[q_t] = acc[q_t] + rest * (ww[i, q] / w_ret)"),
+    "renorm to retained router sum": ("            for j in range(k):\n                w_all += ww[i, j]", "            for j in ret:\n                w_all += ww[i, j]"),
 }
 
 

@@ -501,3 +501,106 @@ def test_storage_matches_projector_ablation_table():
     for fam, (val, unit) in rows.items():
         got = O.table_storage_bytes(48, 128, fam) / units[unit]
         assert f"{got:.2f}" == f"{val:.2f}", fam
+
+
+# ---------------------------------------------------------------- fold safeguards (Appendix C; Eq. dsv4_confidence)
+
+def _safeguard_case():
+    """Three routes of one token: experts 0, 1, 2 with w = (1/2, 1/4, 1/4); the
+    first two are retained.  Source 2: L[2,0] = 3/4, L[2,1] = 1/2, S[2,1] = 2."""
+    ids = np.array([[0, 1, 2]], np.int32)
+    w = np.array([[0.5, 0.25, 0.25]], np.float32)
+    keep = np.array([[True, True, False]])
+    S = np.zeros((3, 3), np.float32)
+    S[2, 0], S[2, 1] = 4.0, 2.0
+    L = np.ones((3, 3), np.float32)
+    L[2, 0], L[2, 1] = 0.75, 0.5
+    return ids, w, keep, S, L
+
+
+def test_safeguards_off_equal_the_main_fold():
+    rng = np.random.default_rng(31)
+    T, N, K, kp = 60, 16, 6, 2
+    ids = np.stack([rng.permutation(N)[:K] for _ in range(T)]).astype(np.int32)
+    w = rng.random((T, K)).astype(np.float32)
+    S = rng.standard_normal((N, N)).astype(np.float32)
+    L = rng.random((N, N)).astype(np.float32)
+    keep = O.select_prefill(ids, w, rng.random(N).astype(np.float32), kp)
+    ref = O.fold_prefill(ids, w, keep, S, L)
+    for kw in ({}, {"loss_cap": float(L.max())}, {"confidence": True}):
+        L_ = np.zeros_like(L) if kw.get("confidence") else L     # c_s = 1 when every loss is 0
+        ref_ = O.fold_prefill(ids, w, keep, S, L_)
+        got = O.fold_prefill_safeguarded(ids, w, keep, S, L_, **kw)
+        np.testing.assert_array_equal(got[0], ref_[0])
+        np.testing.assert_array_equal(got[1].view(np.uint32), ref_[1].view(np.uint32))
+    np.testing.assert_array_equal(O.fold_prefill_safeguarded(ids, w, keep, S, L)[1], ref[1])
+
+
+def test_confidence_split_hand_worked():
+    ids, w, keep, S, L = _safeguard_case()
+    # target: expert 1 (loss 1/2 < 3/4); c = 1/2; target gets 1/4 * 1/2 * 2 = 1/4;
+    # the rest 1/8 goes 2:1 to the retained routes (router weights 1/2 : 1/4)
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, confidence=True)
+    np.testing.assert_array_equal(fw, np.float32([[0.5 + 1 / 12, 0.5 + 1 / 24]]))
+    # with renormalisation the weights sum to the router total 1 (folded total 9/8)
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, confidence=True, renorm=True)
+    np.testing.assert_allclose(fw, [[(7 / 12) * 8 / 9, (13 / 24) * 8 / 9]], rtol=2 ** -23)
+    # a loss above 1 gives c = 0: nothing moves to the target, all of w_s is spread
+    L2 = L.copy()
+    L2[2, 0], L2[2, 1] = 3.0, 1.5
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L2, confidence=True)
+    np.testing.assert_array_equal(fw, np.float32([[0.5 + 1 / 6, 0.25 + 1 / 12]]))
+
+
+def test_loss_cap_hand_worked():
+    ids, w, keep, S, L = _safeguard_case()
+    # cap 0.6 excludes (2, 0) only: the target stays expert 1 -> w1 += 1/4 * 2
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, loss_cap=0.6)
+    np.testing.assert_array_equal(fw, np.float32([[0.5, 0.75]]))
+    # a loss equal to the cap is admissible
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, loss_cap=0.5)
+    np.testing.assert_array_equal(fw, np.float32([[0.5, 0.75]]))
+    # cap below every loss: the omitted route is dropped (Direct Top-K'), and the
+    # renormalised weights keep the router's 2:1 ratio and sum to 1
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, loss_cap=0.4)
+    np.testing.assert_array_equal(fw, np.float32([[0.5, 0.25]]))
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, loss_cap=0.4, renorm=True)
+    np.testing.assert_allclose(fw, [[2 / 3, 1 / 3]], rtol=2 ** -23)
+    # cap 0.7 excludes the cheaper pair's rival only; cap 0.8 keeps both: same target
+    for cap in (0.7, 0.8):
+        _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, loss_cap=cap)
+        np.testing.assert_array_equal(fw, np.float32([[0.5, 0.75]]))
+    # swap the losses: the target becomes expert 0 unless the cap excludes it
+    L3 = L.copy()
+    L3[2, 0], L3[2, 1] = 0.5, 0.75
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L3)
+    np.testing.assert_array_equal(fw, np.float32([[1.5, 0.25]]))
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L3, loss_cap=0.4)
+    np.testing.assert_array_equal(fw, np.float32([[0.5, 0.25]]))
+
+
+def test_renormalisation_preserves_the_routed_weight_sum():
+    rng = np.random.default_rng(32)
+    T, N, K, kp = 80, 32, 8, 3
+    ids = np.stack([rng.permutation(N)[:K] for _ in range(T)]).astype(np.int32)
+    w = rng.dirichlet(np.ones(K), size=T).astype(np.float32)
+    S = rng.random((N, N)).astype(np.float32) * 2            # positive scalars: positive totals
+    L = rng.random((N, N)).astype(np.float32)
+    keep = O.select_prefill(ids, w, rng.random(N).astype(np.float32), kp)
+    for kw in ({"renorm": True}, {"renorm": True, "confidence": True}, {"renorm": True, "loss_cap": 0.5}):
+        _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, **kw)
+        np.testing.assert_allclose(fw.astype(np.float64).sum(1), w.astype(np.float64).sum(1), rtol=K * 2 ** -23)
+    # the confidence split conserves sum_t w_t + sum_s w_s (c_s S[s, t*] + 1 - c_s)
+    _, fw = O.fold_prefill_safeguarded(ids, w, keep, S, L, confidence=True)
+    for i in range(T):
+        ret = [j for j in range(K) if keep[i, j]]
+        exp = sum(float(w[i, j]) for j in ret)
+        for j in range(K):
+            if keep[i, j]:
+                continue
+            s = ids[i, j]
+            lt = [float(L[s, ids[i, q]]) for q in ret]
+            q = ret[int(np.argmin(lt))]
+            c = min(1.0, max(0.0, 1.0 - min(lt)))
+            exp += float(w[i, j]) * (c * float(S[s, ids[i, q]]) + 1.0 - c)
+        assert abs(float(fw[i].astype(np.float64).sum()) - exp) <= 1e-6 * max(1.0, abs(exp))
