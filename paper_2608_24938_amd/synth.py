@@ -186,3 +186,41 @@ def synthetic_tables(n_experts: int, seed: int = 0):
     np.fill_diagonal(L, 0.0)
     h = (np.float32(0.5) + np.float32(1.5) * rng.random(n_experts, dtype=np.float32)).astype(np.float32)
     return S, L, h
+
+
+# ---------------------------------------------------------------------------
+# Directionally aligned experts (a synthetic stand-in for the alignment of
+# expert outputs that the paper observes in trained MoE layers): every routed
+# expert is one base expert with its own output scale c_e and a perturbation,
+#   W_gu[e] = W_gu_base + sigma * N_e,   W_down[e] = c_e * (W_down_base + sigma * M_e),
+# with c_e log-uniform in [1/sqrt(spread), sqrt(spread)] (output norms spread
+# by the factor `spread`).  sigma = 0 gives exact scalar multiples up to the
+# bf16 rounding.  Spawn keys: bases (3, 0) and (3, 1), perturbations (4, e, 0)
+# and (4, e, 1), scales (5,).
+# ---------------------------------------------------------------------------
+
+def aligned_scales(shape: LayerShape, seed: int = 0, spread: float = 3.0) -> np.ndarray:
+    """[N] float64 output scales c_e of the aligned experts."""
+    u = _rng(16 * seed + 0, (5,)).random(shape.n_experts)
+    return np.exp((u - 0.5) * np.log(spread))
+
+
+def aligned_expert_weights(shape: LayerShape, seed: int = 0, sigma: float = 0.3, spread: float = 3.0,
+                           scales=None):
+    """(w_gate_up [N, 2I, d], w_down [N, d, I]) of aligned experts, storage format.
+
+    scales: optional [N] output scales replacing the log-uniform draw."""
+    n, d, inter = shape.n_experts, shape.d, shape.inter
+    base_gu = _rng(16 * seed + 0, (3, 0)).standard_normal((2 * inter, d), dtype=np.float32) * WEIGHT_STD
+    base_dn = _rng(16 * seed + 0, (3, 1)).standard_normal((d, inter), dtype=np.float32) * WEIGHT_STD
+    c = aligned_scales(shape, seed, spread) if scales is None else np.asarray(scales, dtype=np.float64)
+    gu = np.empty((n, 2 * inter, d), dtype=np.uint16 if shape.dtype == "bf16" else np.float32)
+    dn = np.empty((n, d, inter), dtype=gu.dtype)
+    for e in range(n):
+        g = base_gu + np.float32(sigma * WEIGHT_STD) * _rng(16 * seed + 0, (4, e, 0)).standard_normal(
+            base_gu.shape, dtype=np.float32)
+        w = (base_dn + np.float32(sigma * WEIGHT_STD) * _rng(16 * seed + 0, (4, e, 1)).standard_normal(
+            base_dn.shape, dtype=np.float32)) * np.float32(c[e])
+        gu[e] = _bf16_bits_inplace(g) if shape.dtype == "bf16" else g
+        dn[e] = _bf16_bits_inplace(w) if shape.dtype == "bf16" else w
+    return gu, dn
