@@ -71,6 +71,8 @@ READINGS = {
            "to their router weights.",
     "R24": "Renormalisation: retained weights scaled by (sum of the K router weights) / "
            "(sum of the folded weights) when that sum is positive.",
+    "R26": "Diagonal projectors: no clipping; unobserved pair d = 0, loss 1e30; self pair d = 1, "
+           "loss 0; a zero denominator gives d_n = 0.",
 }
 
 FIXED_POINT_BITS = 40       # R6
@@ -620,6 +622,131 @@ def calibrate(layer: Layer, x_cal, top_k: int, lam: float = DEFAULT_LAMBDA,
         h[~observed] = h[observed].mean()
     stats = dict(A=A, V=V, C=C, n=n, S64=S, L64=Lo, h64=h)
     return S.astype(np.float32), Lo.astype(np.float32), h.astype(np.float32), stats
+
+
+# ---------------------------------------------------------------------------
+# Diagonal projector family  (Appendix A, Eq. appendix_diagonal_projector; the
+# unfused reconstruction path of the projector ablation)
+# ---------------------------------------------------------------------------
+
+def calibrate_diagonal(layer: Layer, x_cal, top_k: int, lam: float = DEFAULT_LAMBDA,
+                       mode: str = "corouted", logits=None):
+    """Per-dimension projectors d_{s->t} = sum_i w_i (v_i . u_i) / (sum_i w_i (v_i . v_i) + lambda)
+    (element-wise, Eq. appendix_diagonal_projector) with w_i = ||u_i||, and their
+    normalised reconstruction loss sum_i w_i ||u_i - d . v_i||^2 / (sum_i w_i ||u_i||^2 + eps)
+    (Eq. appendix_projection_loss with the diagonal map; R26: no clipping; an
+    unobserved pair has d = 0 and loss 1e30; d_{s->s} = 1, loss 0).
+
+    Returns (Dg [N, N, d] float32, Ld [N, N] float32, stats dict with float64 A, V
+    [N, N, d], C, n)."""
+    x = _f64(x_cal)
+    nn = layer.n_experts
+    dd = x.shape[1]
+    if logits is None:
+        logits = router_logits(x, layer.w_router, layer.router_bias)
+    ids = topk_ids(logits, top_k)
+    m = x.shape[0]
+    if mode == "corouted":
+        evaluated = [list(map(int, ids[i])) for i in range(m)]
+    elif mode == "common":
+        evaluated = [list(range(nn)) for _ in range(m)]
+    else:
+        raise ValueError(mode)
+    outputs = {}
+    for e in range(nn):
+        tok = [i for i in range(m) if e in evaluated[i]]
+        if tok:
+            gu, dn = layer.expert(e)
+            outputs[e] = dict(zip(tok, expert_forward(x[tok], gu, dn)))
+    A = np.zeros((nn, nn, dd))
+    V = np.zeros((nn, nn, dd))
+    C = np.zeros((nn, nn))
+    n = np.zeros((nn, nn), dtype=np.int64)
+    for i in range(m):
+        ev = evaluated[i]
+        for s in ev:
+            u = outputs[s][i]
+            wi = math.sqrt(float(u @ u))
+            for t in ev:
+                if t == s:
+                    continue
+                v = outputs[t][i]
+                A[s, t] += wi * (v * u)
+                V[s, t] += wi * (v * v)
+                C[s, t] += wi * float(u @ u)
+                n[s, t] += 1
+    Dg = np.zeros((nn, nn, dd))
+    Ld = np.full((nn, nn), UNOBSERVED_LOSS)
+    for s in range(nn):
+        for t in range(nn):
+            if s == t:
+                Dg[s, t], Ld[s, t] = 1.0, 0.0
+                continue
+            if n[s, t] == 0:
+                continue
+            den = V[s, t] + lam
+            dv = np.where(den != 0.0, A[s, t] / np.where(den != 0.0, den, 1.0), 0.0)
+            Dg[s, t] = dv
+            resid = C[s, t] - 2.0 * float(dv @ A[s, t]) + float((dv * dv) @ V[s, t])
+            Ld[s, t] = max(0.0, resid) / (C[s, t] + EPSILON)
+    return Dg.astype(np.float32), Ld.astype(np.float32), dict(A=A, V=V, C=C, n=n, D64=Dg, L64=Ld)
+
+
+def fold_prefill_diagonal(ids, w, keep, Ld):
+    """Prefill selection with diagonal projectors: the retained routes keep their
+    router weights, and each omitted route s (route order) is assigned to the
+    first minimum of Ld[s, t] over the retained routes (Eq.
+    appendix_minimum_loss_assignment with the diagonal family's loss).
+
+    Returns (out_ids [T, K'] int32, out_w [T, K'] float32: the retained routes in
+    route order, and fold [T] lists of (source expert, weight, retained position))."""
+    ids = np.asarray(ids)
+    t, k = ids.shape
+    k_out = int(np.asarray(keep)[0].sum()) if t else 0
+    out_ids = np.zeros((t, k_out), dtype=np.int32)
+    out_w = np.zeros((t, k_out), dtype=np.float32)
+    Ld = np.asarray(Ld, dtype=np.float32)
+    folds = []
+    for i in range(t):
+        ret = [j for j in range(k) if keep[i, j]]
+        ret_experts = [int(ids[i, j]) for j in ret]
+        fl = []
+        for j in range(k):
+            if keep[i, j]:
+                continue
+            s = int(ids[i, j])
+            tgt = min_loss_target(Ld[s], ret_experts)
+            fl.append((s, float(np.float32(w[i, j])), ret_experts.index(tgt)))
+        for c, j in enumerate(ret):
+            out_ids[i, c] = ids[i, j]
+            out_w[i, c] = w[i, j]
+        folds.append(fl)
+    return out_ids, out_w, folds
+
+
+def diagonal_output(layer: Layer, x, out_ids, out_w, folds, Dg) -> np.ndarray:
+    """y_i = sum over retained routes t of (w_t 1 + sum of w_s d_{s->t} over the
+    omitted s folded onto t) . E_t(x_i), plus the shared expert (Eq. folded_moe
+    with the diagonal map acting on the target's output)."""
+    x = _f64(x)
+    Dg = _f64(Dg)
+    t = x.shape[0]
+    y = np.zeros_like(x)
+    for e in range(layer.n_experts):
+        tok, slot = np.nonzero(np.asarray(out_ids) == e)
+        if tok.size == 0:
+            continue
+        gu, dn = layer.expert(e)
+        out = expert_forward(x[tok], gu, dn)
+        for r, (i, q) in enumerate(zip(tok, slot)):
+            coef = np.full(x.shape[1], float(out_w[i, q]))
+            for s, ws, qq in folds[i]:
+                if qq == q:
+                    coef = coef + ws * Dg[s, e]
+            y[i] += coef * out[r]
+    if layer.ws_gate_up is not None:
+        y += expert_forward(x, layer.ws_gate_up, layer.ws_down)
+    return y
 
 
 def table_storage_bytes(n_layers: int, n_experts: int, family: str) -> int:

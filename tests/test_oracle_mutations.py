@@ -51,6 +51,13 @@ MUTANTS = {
     "confidence not clipped": ("c = min(1.0, max(0.0, 1.0 - float(L[s, ids[i, q_t]])))", "c = 1.0 - float(L[s, ids[i, q_t]])"),
     "confidence spread uniform": ("acc[q] = acc[q] + rest * (ww[i, q] / w_ret)", "acc[q] = acc[q] + rest / len(ret)"),
     "confidence remainder to target": ("acc[q] = acc[q] + rest * (ww[i, q] / w_ret)", "acc[q_t] = acc[q_t] + rest * (ww[i, q] / w_ret)"),
+    "diagonal numerator uses target energy": ("A[s, t] += wi * (v * u)", "A[s, t] += wi * (v * v)"),
+    "diagonal ridge dropped": ("            den = V[s, t] + lam\n            dv =", "            den = V[s, t]\n            dv ="),
+    "diagonal loss sign": ("resid = C[s, t] - 2.0 * float(dv @ A[s, t])", "resid = C[s, t] + 2.0 * float(dv @ A[s, t])"),
+    "diagonal weight is target norm": ("            u = outputs[s][i]\n            wi = math.sqrt(float(u @ u))",
+                                       "            u = outputs[s][i]\n            wi = math.sqrt(float(outputs[ev[-1]][i] @ outputs[ev[-1]][i]))"),
+    "diagonal output ignores folds": ("coef = coef + ws * Dg[s, e]", "coef = coef"),
+    "diagonal map of the source expert": ("coef = coef + ws * Dg[s, e]", "coef = coef + ws * Dg[e, s]"),
     "renorm to retained router sum": ("            for j in range(k):\n                w_all += ww[i, j]", "            for j in ret:\n                w_all += ww[i, j]"),
 }
 

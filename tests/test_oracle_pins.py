@@ -604,3 +604,95 @@ def test_renormalisation_preserves_the_routed_weight_sum():
             c = min(1.0, max(0.0, 1.0 - min(lt)))
             exp += float(w[i, j]) * (c * float(S[s, ids[i, q]]) + 1.0 - c)
         assert abs(float(fw[i].astype(np.float64).sum()) - exp) <= 1e-6 * max(1.0, abs(exp))
+
+
+# ---------------------------------------------------------------- diagonal projector (Eq. appendix_diagonal_projector)
+
+def _diag_layer(rng, n=4, d=6, inter=5, shared_gate=False):
+    gu = rng.standard_normal((n, 2 * inter, d)) * 0.5
+    if shared_gate:
+        gu[:] = gu[0]
+    dn = rng.standard_normal((n, d, inter)) * 0.5
+    wr = rng.standard_normal((n, d)) * 0.5
+    return O.Layer(w_router=wr, w_gate_up=gu, w_down=dn)
+
+
+def test_diagonal_projector_is_per_dimension_weighted_ridge():
+    rng = np.random.default_rng(41)
+    layer = _diag_layer(rng)
+    x = rng.standard_normal((40, 6))
+    lam = 0.3
+    Dg, Ld, st = O.calibrate_diagonal(layer, x, top_k=3, lam=lam, mode="common")
+    U = np.stack([O.expert_forward(x, *layer.expert(e)) for e in range(4)])      # [N, m, d]
+    s, t = 2, 0
+    wv = np.linalg.norm(U[s], axis=1)
+    for nd in range(6):
+        # minimise sum_i w_i (u_in - c v_in)^2 + lam c^2 as a stacked least-squares problem
+        a = np.concatenate([np.sqrt(wv) * U[t][:, nd], [np.sqrt(lam)]])[:, None]
+        b = np.concatenate([np.sqrt(wv) * U[s][:, nd], [0.0]])
+        c = np.linalg.lstsq(a, b, rcond=None)[0][0]
+        assert abs(st["D64"][s, t, nd] - c) <= 1e-10 * max(1.0, abs(c))
+    # the loss is the weighted residual of the diagonal map, normalised by the source energy
+    resid = float((wv * ((U[s] - st["D64"][s, t] * U[t]) ** 2).sum(1)).sum())
+    energy = float((wv * (U[s] ** 2).sum(1)).sum())
+    assert abs(st["L64"][s, t] - resid / (energy + O.EPSILON)) <= 1e-9 * max(1.0, st["L64"][s, t])
+    assert np.all(Dg[np.arange(4), np.arange(4)] == 1.0) and np.all(Ld[np.arange(4), np.arange(4)] == 0.0)
+
+
+def test_diagonal_recovers_per_dimension_scales_exactly():
+    # target outputs scaled per hidden dimension: u = c . v (c a vector of powers of two):
+    # with lambda = 0 the diagonal projector is exactly c with zero loss, while the
+    # scalar projector cannot represent it (positive loss)
+    rng = np.random.default_rng(42)
+    layer = _diag_layer(rng, shared_gate=True)
+    cvec = np.array([0.5, 2.0, -1.0, 4.0, 0.25, -2.0])
+    layer.w_down[1] = cvec[:, None] * layer.w_down[0]
+    x = rng.standard_normal((30, 6))
+    Dg, Ld, _ = O.calibrate_diagonal(layer, x, top_k=4, lam=0.0, mode="common")
+    np.testing.assert_array_equal(Dg[1, 0], cvec.astype(np.float32))
+    assert Ld[1, 0] <= 1e-12
+    S, L, _, _ = O.calibrate(layer, x, top_k=4, lam=0.0, clip=0.0, mode="common")
+    assert L[1, 0] > 0.1
+
+
+def test_diagonal_fold_reproduces_the_full_output_for_exact_maps():
+    # experts 2 and 3 are exact per-dimension multiples of experts 0 and 1: with the
+    # calibrated diagonal maps, folding them onto 0 and 1 gives the full output
+    rng = np.random.default_rng(43)
+    layer = _diag_layer(rng)
+    c2 = np.array([0.5, 2.0, 1.0, -1.0, 0.25, 4.0])
+    c3 = np.array([2.0, -0.5, 1.0, 0.5, 1.0, 2.0])
+    layer.w_gate_up[2] = layer.w_gate_up[0]
+    layer.w_gate_up[3] = layer.w_gate_up[1]
+    layer.w_down[2] = c2[:, None] * layer.w_down[0]
+    layer.w_down[3] = c3[:, None] * layer.w_down[1]
+    x = rng.standard_normal((30, 6))
+    Dg, Ld, _ = O.calibrate_diagonal(layer, x, top_k=4, lam=0.0, mode="common")
+    ids = np.array([[0, 1, 2, 3]] * 30, np.int32)
+    w = np.tile(np.float32([0.4, 0.3, 0.2, 0.1]), (30, 1))
+    keep = np.array([[True, True, False, False]] * 30)
+    oi, ow, folds = O.fold_prefill_diagonal(ids, w, keep, Ld)
+    assert [(s, q) for s, _, q in folds[0]] == [(2, 0), (3, 1)]
+    y = O.diagonal_output(layer, x, oi, ow, folds, Dg)
+    ref = O.moe_output(layer, x, ids, w)
+    assert np.abs(y - ref).max() <= 1e-6 * np.abs(ref).max()
+
+
+def test_diagonal_with_uniform_maps_equals_the_scalar_fold():
+    # a diagonal map c . 1 acts like the scalar c: same targets (same loss table),
+    # same output as Eq. prefill_fold
+    rng = np.random.default_rng(44)
+    layer = _diag_layer(rng, n=6, d=5, inter=4)
+    x = rng.standard_normal((20, 5))
+    S = rng.standard_normal((6, 6)).astype(np.float32)
+    L = rng.random((6, 6)).astype(np.float32)
+    Dg = np.repeat(S[:, :, None], 5, axis=2)
+    lg = O.router_logits(x, layer.w_router)
+    ids, w = O.route(lg, 4)
+    keep = O.select_prefill(ids, w, rng.random(6).astype(np.float32), 2)
+    oi, ow, folds = O.fold_prefill_diagonal(ids, w, keep, L)
+    y = O.diagonal_output(layer, x, oi, ow, folds, Dg)
+    fi, fw = O.fold_prefill(ids, w, keep, S, L)
+    np.testing.assert_array_equal(oi, fi)
+    ref = O.moe_output(layer, x, fi, fw)
+    assert np.abs(y - ref).max() <= 1e-6 * np.abs(ref).max()
