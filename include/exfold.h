@@ -68,9 +68,13 @@ enum {
   EXFOLD_PHASE_DENSE = 0,    /* unfolded layer on the Top-K routes (Eq. moe_output)  */
   EXFOLD_PHASE_PREFILL = 1,  /* per-token K' budget (Eq. prefill_budget/prefill_fold) */
   EXFOLD_PHASE_DECODE = 2,   /* per-batch pool of D (Eq. decode_budget/decode_remap)  */
-  EXFOLD_PHASE_DECODE_STATIC = 3  /* static pool of D: remap with precomputed tables
+  EXFOLD_PHASE_DECODE_STATIC = 3, /* static pool of D: remap with precomputed tables
                                      (Appendix B, Eq. appendix_decode_static_budget,
                                      Eq. appendix_decode_remap); see exfold_static_pool */
+  EXFOLD_PHASE_PREFILL_DIAG = 4   /* per-token K' budget with diagonal projectors on the
+                                     unfused path (Appendix A,
+                                     Eq. appendix_diagonal_projector); see
+                                     exfold_calibrate_diagonal */
 };
 
 enum {
@@ -123,6 +127,9 @@ typedef struct exfold_tables {
   const float *scl;    /* [N]    float32: its scale, or NULL                  */
   float loss_cap;      /* prefill: cap of EXFOLD_FOLD_LOSS_CAP                */
   int32_t fold_flags;  /* prefill: EXFOLD_FOLD_* safeguards, 0 = none         */
+  const float *Dg;     /* [N, N, d] diagonal maps d_{s->t} (Dg[(s*N+t)*d+n]) for
+                          EXFOLD_PHASE_PREFILL_DIAG, whose L is then the diagonal
+                          loss table; NULL otherwise                          */
 } exfold_tables;
 
 /* Stage boundaries at which exfold_moe_forward records the optional events. */
@@ -238,6 +245,10 @@ size_t exfold_moe_workspace_size(const exfold_layer *layer, int64_t T, int32_t p
  * grouped SwiGLU expert GEMMs over the retained routes only, weighted combine.
  *   x   [T, d] input tokens, y [T, d] output (same dtype as the layer).
  *   tables may be NULL for EXFOLD_PHASE_DENSE; budget is ignored there.
+ *   EXFOLD_PHASE_PREFILL_DIAG needs tables->h, L (the diagonal loss) and Dg from
+ *   exfold_calibrate_diagonal: the K' routes of largest w*h execute with their
+ *   router weights w_t, each omitted route s goes to the first minimum of L[s, t]
+ *   over them, and y_i = sum_t (w_t + sum of w_s Dg[s, t]) . E_t(x_i) (+ shared).
  *   EXFOLD_PHASE_DECODE_STATIC needs tables->tgt/scl from exfold_static_pool
  *   (budget = its D) and leaves the debug pool/pool_size/tgt_ids/tgt_scale
  *   untouched; a slot of source s becomes (tgt[s], w * scl[s]) unless tgt[s] == s.
@@ -265,7 +276,8 @@ exfold_status exfold_moe_execute(const exfold_layer *layer, const void *x, int64
                                  void *y, const exfold_debug *debug, void *ws, size_t ws_bytes,
                                  void *stream);
 
-/* Bytes of workspace exfold_calibrate_projectors needs for m calibration tokens. */
+/* Bytes of workspace exfold_calibrate_projectors (and exfold_calibrate_diagonal)
+ * needs for m calibration tokens. */
 size_t exfold_calibrate_workspace_size(const exfold_layer *layer, int64_t m, int32_t mode);
 
 /*
@@ -291,6 +303,22 @@ exfold_status exfold_calibrate_projectors(const exfold_layer *layer, const void 
 
 /* Static text for a status code. */
 const char *exfold_status_str(exfold_status status);
+
+/*
+ * Diagonal projector calibration (Appendix A, Eq. appendix_diagonal_projector;
+ * the unfused family of the projector ablation).  Routing, evaluated pairs and
+ * the weight w = ||u||_2 are those of exfold_calibrate_projectors.  Per ordered
+ * pair (s, t), in token order and float64, per hidden dimension n:
+ *   A_n = sum w v_n u_n, V_n = sum w v_n^2, C = sum w ||u||^2;
+ *   Dg[(s*N+t)*d+n] = A_n / (V_n + lambda) (0 where that denominator is 0),
+ *   Ld[s*N+t] = max(0, C - 2 sum_n Dg_n A_n + sum_n Dg_n^2 V_n) / (C + 1e-12).
+ *   Unobserved pairs: Dg = 0, Ld = 1e30.  Self pairs: Dg = 1, Ld = 0.  No clip.
+ *   Outputs Dg [N, N, d] and Ld [N, N] float32 (rounded once).  lambda >= 0.
+ *   ws: exfold_calibrate_workspace_size(layer, m, mode) bytes.
+ */
+exfold_status exfold_calibrate_diagonal(const exfold_layer *layer, const void *x_cal, int64_t m,
+                                        double lambda, int32_t mode, float *Dg, float *Ld, void *ws,
+                                        size_t ws_bytes, void *stream);
 
 #ifdef __cplusplus
 }

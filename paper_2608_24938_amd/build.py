@@ -31,7 +31,7 @@ FLAGS = [
     "-mllvm", "-disable-promote-alloca-to-lds",
     f"-I{INCLUDE}", f"-I{CSRC}",
 ]
-SOURCES = ["exfold_api.hip", "k_route.hip", "k_permute.hip", "k_gemm.hip", "k_calib.hip"]
+SOURCES = ["exfold_api.hip", "k_route.hip", "k_permute.hip", "k_gemm.hip", "k_calib.hip", "k_diag.hip"]
 
 
 def _run(cmd):

@@ -180,7 +180,8 @@ exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
 struct ForwardPlan {
   int T = 0, N = 0, K = 0, k_out = 0, phase = 0, budget = 0, dcap = 0, P = 1;
   size_t o_logits = 0, o_topk_ids = 0, o_topk_w = 0, o_keep = 0, o_pool = 0, o_pool_size = 0,
-         o_tgt = 0, o_scl = 0, o_fold_ids = 0, o_fold_w = 0;
+         o_tgt = 0, o_scl = 0, o_fold_ids = 0, o_fold_w = 0, o_om_src = 0, o_om_w = 0, o_om_q = 0,
+         o_wret = 0;
   ExecPlan ex;
   size_t total = 0;
 };
@@ -190,7 +191,7 @@ exfold_status plan_forward(const exfold_layer *L, int64_t T, int32_t phase, int6
   exfold_status st = check_layer(L);
   if (st != EXFOLD_OK) return st;
   if (phase != EXFOLD_PHASE_DENSE && phase != EXFOLD_PHASE_PREFILL && phase != EXFOLD_PHASE_DECODE &&
-      phase != EXFOLD_PHASE_DECODE_STATIC)
+      phase != EXFOLD_PHASE_DECODE_STATIC && phase != EXFOLD_PHASE_PREFILL_DIAG)
     return EXFOLD_ERR_ARG;
   st = check_routing(T, L->n_experts, L->top_k);
   if (st != EXFOLD_OK) return st;
@@ -200,7 +201,8 @@ exfold_status plan_forward(const exfold_layer *L, int64_t T, int32_t phase, int6
   p.K = (int)L->top_k;
   p.phase = phase;
   p.budget = (int)(budget > (1 << 20) ? (1 << 20) : budget);
-  p.k_out = (phase == EXFOLD_PHASE_PREFILL) ? (p.budget < p.K ? p.budget : p.K) : p.K;
+  const bool per_token = phase == EXFOLD_PHASE_PREFILL || phase == EXFOLD_PHASE_PREFILL_DIAG;
+  p.k_out = per_token ? (p.budget < p.K ? p.budget : p.K) : p.K;
   p.dcap = (p.budget < p.N) ? p.budget : p.N;
   p.P = router_splits(L->dtype, p.T, p.N, (int)L->d);
   Carver c;
@@ -214,11 +216,17 @@ exfold_status plan_forward(const exfold_layer *L, int64_t T, int32_t phase, int6
   p.o_scl = c.take(sizeof(float) * p.N);
   p.o_fold_ids = c.take(sizeof(int32_t) * (size_t)p.T * p.k_out);
   p.o_fold_w = c.take(sizeof(float) * (size_t)p.T * p.k_out);
+  if (phase == EXFOLD_PHASE_PREFILL_DIAG) {
+    p.o_om_src = c.take(sizeof(int32_t) * (size_t)p.T * p.K);
+    p.o_om_w = c.take(sizeof(float) * (size_t)p.T * p.K);
+    p.o_om_q = c.take(sizeof(int32_t) * (size_t)p.T * p.K);
+    p.o_wret = c.take(sizeof(float) * (size_t)p.T * p.k_out);
+  }
   int active = p.N;
   if (phase == EXFOLD_PHASE_DECODE || phase == EXFOLD_PHASE_DECODE_STATIC) active = p.dcap;
   if (p.T * p.k_out < active) active = p.T * p.k_out;
   if (L->shared_inter > 0) active += 1;
-  plan_exec(L, phase, p.T, p.k_out, true, false, active, c, p.ex);
+  plan_exec(L, phase, p.T, p.k_out, true, phase == EXFOLD_PHASE_PREFILL_DIAG, active, c, p.ex);
   p.total = c.off;
   return EXFOLD_OK;
 }
@@ -410,6 +418,8 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
   if (st != EXFOLD_OK) return st;
   if (phase == EXFOLD_PHASE_DECODE_STATIC) {
     if (!tables || !tables->tgt || !tables->scl) return EXFOLD_ERR_NULL;
+  } else if (phase == EXFOLD_PHASE_PREFILL_DIAG) {
+    if (!tables || !tables->L || !tables->h || !tables->Dg) return EXFOLD_ERR_NULL;
   } else if (phase != EXFOLD_PHASE_DENSE && (!tables || !tables->S || !tables->L || !tables->h)) {
     return EXFOLD_ERR_NULL;
   }
@@ -450,6 +460,11 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
     e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.k_out, tables->h, tables->S,
                             tables->L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s,
                             tables->loss_cap, tables->fold_flags);
+  } else if (phase == EXFOLD_PHASE_PREFILL_DIAG) {
+    e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.k_out, tables->h, nullptr,
+                            tables->L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s, 0.f, 0,
+                            at<int32_t>(ws, p.o_om_src), at<float>(ws, p.o_om_w),
+                            at<int32_t>(ws, p.o_om_q), at<float>(ws, p.o_wret));
   } else {
     const bool stat = phase == EXFOLD_PHASE_DECODE_STATIC;
     e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,
@@ -473,8 +488,21 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
   }
   if (e != hipSuccess) return EXFOLD_ERR_DEVICE;
   record(dbg.events, EXFOLD_EV_FOLD, s);
-  return run_exec(layer, p.ex, x, exec_ids, exec_w, y, ws, dbg.offsets, dbg.row_slot, false, s,
-                  dbg.events, permuted);
+  if (phase != EXFOLD_PHASE_PREFILL_DIAG)
+    return run_exec(layer, p.ex, x, exec_ids, exec_w, y, ws, dbg.offsets, dbg.row_slot, false, s,
+                    dbg.events, permuted);
+  // diagonal projectors: unweighted expert rows, then the element-wise combine
+  st = run_exec(layer, p.ex, x, exec_ids, exec_w, nullptr, ws, dbg.offsets, dbg.row_slot, true, s,
+                dbg.events);
+  if (st != EXFOLD_OK) return st;
+  const PermBuffers pb = perm_buffers(p.ex, ws, dbg.offsets, dbg.row_slot);
+  if (launch_diag_combine(layer->dtype, at<float>(ws, p.ex.o_Y), pb.slot_row, fold_ids,
+                          at<float>(ws, p.o_wret), at<int32_t>(ws, p.o_om_src), at<float>(ws, p.o_om_w),
+                          at<int32_t>(ws, p.o_om_q), tables->Dg, p.T, p.N, p.K, p.k_out,
+                          (int)layer->d, p.ex.t_shared > 0 ? p.ex.R : -1, y, s) != hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  record(dbg.events, EXFOLD_EV_END, s);
+  return EXFOLD_OK;
 }
 
 size_t exfold_execute_workspace_size(const exfold_layer *layer, int64_t T, int64_t k_out) {
@@ -544,6 +572,47 @@ exfold_status exfold_calibrate_projectors(const exfold_layer *layer, const void 
   }
   if (launch_calib_finalize(gram, pos, p.m, p.N, p.kr, lambda, clip, S, L, h, pair_stats, s) !=
       hipSuccess)
+    return EXFOLD_ERR_DEVICE;
+  return EXFOLD_OK;
+}
+
+exfold_status exfold_calibrate_diagonal(const exfold_layer *layer, const void *x_cal, int64_t m,
+                                        double lambda, int32_t mode, float *Dg, float *Ld, void *ws,
+                                        size_t ws_bytes, void *stream) {
+  CalibPlan p;
+  exfold_status st = plan_calibrate(layer, m, mode, p);
+  if (st != EXFOLD_OK) return st;
+  if (!(lambda >= 0.0)) return EXFOLD_ERR_ARG;
+  if (!Dg || !Ld) return EXFOLD_ERR_NULL;
+  if (m > 0 && !x_cal) return EXFOLD_ERR_NULL;
+  st = check_ws(ws, ws_bytes, p.total);
+  if (st != EXFOLD_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  float *logits = at<float>(ws, p.o_logits);
+  int32_t *topk_ids = at<int32_t>(ws, p.o_topk_ids);
+  float *topk_w = at<float>(ws, p.o_topk_w);
+  int32_t *route_ids = at<int32_t>(ws, p.o_route_ids);
+  float *route_w = at<float>(ws, p.o_route_w);
+  int16_t *pos = at<int16_t>(ws, p.o_pos);
+  double *gram = at<double>(ws, p.o_gram);
+  if (p.m > 0) {
+    if (launch_router_logits(layer->dtype, x_cal, layer->w_router, p.m, p.N, (int)layer->d, p.P,
+                             logits, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+    if (launch_route_tokens(logits, p.P, layer->router_bias, nullptr, p.m, p.N, p.K, p.K, nullptr,
+                            nullptr, nullptr, topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr,
+                            s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+    if (launch_calib_routes(topk_ids, p.m, p.N, p.K, mode, route_ids, route_w, pos, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+    st = run_exec(layer, p.ex, x_cal, route_ids, route_w, nullptr, ws, nullptr, nullptr, true, s);
+    if (st != EXFOLD_OK) return st;
+    if (launch_calib_gram(at<float>(ws, p.ex.o_Y), at<int32_t>(ws, p.ex.o_slot_row), p.m, p.kr,
+                          (int)layer->d, gram, s) != hipSuccess)
+      return EXFOLD_ERR_DEVICE;
+  }
+  if (launch_diag_stats(at<float>(ws, p.ex.o_Y), at<int32_t>(ws, p.ex.o_slot_row), gram, pos, p.m, p.N,
+                        p.kr, (int)layer->d, lambda, Dg, Ld, s) != hipSuccess)
     return EXFOLD_ERR_DEVICE;
   return EXFOLD_OK;
 }

@@ -226,7 +226,9 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
     float *__restrict__ logits_out, int T, int N, int K, int k_pre, const float *__restrict__ h,
     const float *__restrict__ S, const float *__restrict__ L, int32_t *__restrict__ topk_ids,
     float *__restrict__ topk_w, uint8_t *__restrict__ keep, const uint8_t *__restrict__ keep_in,
-    int32_t *__restrict__ fold_ids, float *__restrict__ fold_w, float loss_cap, int flags) {
+    int32_t *__restrict__ fold_ids, float *__restrict__ fold_w, float loss_cap, int flags,
+    int32_t *__restrict__ om_src, float *__restrict__ om_w, int32_t *__restrict__ om_q,
+    float *__restrict__ wret) {
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // uniform per wave
@@ -290,12 +292,31 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
         }
       }
     }
-    if (tgt_lane >= 0) {
+    if (tgt_lane >= 0 && !om_src) {
       double c = 1.0;
       if (conf) c = fmin(1.0, fmax(0.0, __dsub_rn(1.0, (double)best)));
       contrib = __dmul_rn(__dmul_rn((double)my_w, c), (double)S[(size_t)my_id * N + ids[tgt_lane]]);
       if (conf) rest = __dmul_rn((double)my_w, __dsub_rn(1.0, c));
     }
+  }
+  // Diagonal projectors (unfused path): the retained routes execute with weight
+  // 1 and keep their router weights aside; each omitted route records its
+  // source, weight and the position of its target among the retained routes.
+  if (om_src) {
+    const int k_out = min(k_pre, K);
+    const int p = __popcll(kmask & lanemask_lt(lane));
+    if (kept && p < k_out) {
+      fold_ids[(size_t)t * k_out + p] = my_id;
+      fold_w[(size_t)t * k_out + p] = 1.0f;
+      wret[(size_t)t * k_out + p] = my_w;
+    }
+    if (lane < K) {
+      const int qpos = (!kept && tgt_lane >= 0) ? __popcll(kmask & lanemask_lt(tgt_lane)) : -1;
+      om_src[(size_t)t * K + lane] = kept ? -1 : my_id;
+      om_w[(size_t)t * K + lane] = my_w;
+      om_q[(size_t)t * K + lane] = qpos;
+    }
+    return;
   }
   // Coalesce onto each retained route, omitted routes in route order: the
   // target's share, then (confidence split) the spread w_s (1 - c_s) w_t / W_ret.
@@ -336,11 +357,12 @@ hipError_t launch_route_tokens(const float *part, int P, const float *bias, floa
                                int N, int K, int k_pre, const float *h, const float *S, const float *L,
                                int32_t *topk_ids, float *topk_w, uint8_t *keep,
                                const uint8_t *keep_in, int32_t *fold_ids, float *fold_w,
-                               hipStream_t s, float loss_cap, int flags) {
+                               hipStream_t s, float loss_cap, int flags, int32_t *om_src,
+                               float *om_w, int32_t *om_q, float *wret) {
   if (T <= 0) return hipSuccess;
   route_tokens_kernel<<<(T + 3) / 4, 256, 0, s>>>(part, P, bias, logits_out, T, N, K, k_pre, h, S, L,
                                                   topk_ids, topk_w, keep, keep_in, fold_ids, fold_w,
-                                                  loss_cap, flags);
+                                                  loss_cap, flags, om_src, om_w, om_q, wret);
   return hipGetLastError();
 }
 

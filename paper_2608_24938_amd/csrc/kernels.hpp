@@ -20,7 +20,9 @@ hipError_t launch_route_tokens(const float *part, int P, const float *bias, floa
                                int N, int K, int k_pre, const float *h, const float *S, const float *L,
                                int32_t *topk_ids, float *topk_w, uint8_t *keep,
                                const uint8_t *keep_in, int32_t *fold_ids, float *fold_w,
-                               hipStream_t s, float loss_cap = 0.f, int flags = 0);
+                               hipStream_t s, float loss_cap = 0.f, int flags = 0,
+                               int32_t *om_src = nullptr, float *om_w = nullptr,
+                               int32_t *om_q = nullptr, float *wret = nullptr);
 // Decode pool (if do_pool) and per-source tables + per-slot remap (if out_ids).
 hipError_t launch_decode_pool_fold(const int32_t *ids, const float *w, int B, int N, int K, int D,
                                    const float *h, const float *S, const float *L, bool do_pool,
@@ -94,6 +96,17 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
                                hipStream_t s, hipEvent_t ev_mid = nullptr);
 hipError_t launch_combine(int dtype, const float *Y, int ksplit, int rows, const int32_t *slot_row,
                           int T, int k_out, int d, int shared_base, void *y, hipStream_t s);
+
+// ---- diagonal projectors (k_diag.hip) ----
+// Per-pair per-dimension statistics -> Dg [N, N, d] and the diagonal loss Ld [N, N].
+hipError_t launch_diag_stats(const float *Y, const int32_t *slot_row, const double *gram,
+                             const int16_t *pos, int m, int N, int kr, int d, double lambda, float *Dg,
+                             float *Ld, hipStream_t s);
+// y from the unweighted expert rows and the diagonal fold lists.
+hipError_t launch_diag_combine(int dtype, const float *Yr, const int32_t *slot_row, const int32_t *ids,
+                               const float *wret, const int32_t *om_src, const float *om_w,
+                               const int32_t *om_q, const float *Dg, int T, int N, int K, int k_out,
+                               int d, int shared_base, void *y, hipStream_t s);
 
 // ---- calibration (k_calib.hip) ----
 hipError_t launch_calib_routes(const int32_t *topk_ids, int m, int N, int K, int mode,

@@ -19,13 +19,14 @@ _lib = None
 
 OK, ERR_NULL, ERR_SHAPE, ERR_BUDGET, ERR_DTYPE, ERR_WORKSPACE, ERR_DEVICE, ERR_UNSUPPORTED, ERR_ARG = range(9)
 F32, BF16 = 0, 1
-PHASE = {"dense": 0, "prefill": 1, "decode": 2, "decode_static": 3}
+PHASE = {"dense": 0, "prefill": 1, "decode": 2, "decode_static": 3, "prefill_diag": 4}
 CAL_MODE = {"corouted": 0, "common": 1}
 
 EXPORTED = [
     "exfold_select_prefill", "exfold_select_decode_pool", "exfold_fold_gates", "exfold_static_pool",
     "exfold_moe_workspace_size", "exfold_moe_forward", "exfold_execute_workspace_size",
     "exfold_moe_execute", "exfold_calibrate_workspace_size", "exfold_calibrate_projectors",
+    "exfold_calibrate_diagonal",
     "exfold_status_str",
 ]
 
@@ -47,7 +48,7 @@ class _Layer(ctypes.Structure):
 class _Tables(ctypes.Structure):
     _fields_ = [("S", ctypes.c_void_p), ("L", ctypes.c_void_p), ("h", ctypes.c_void_p),
                 ("tgt", ctypes.c_void_p), ("scl", ctypes.c_void_p), ("loss_cap", ctypes.c_float),
-                ("fold_flags", ctypes.c_int32)]
+                ("fold_flags", ctypes.c_int32), ("Dg", ctypes.c_void_p)]
 
 
 FOLD_LOSS_CAP, FOLD_RENORM, FOLD_CONFIDENCE = 1, 2, 4
@@ -93,6 +94,7 @@ def lib() -> ctypes.CDLL:
             "exfold_moe_execute": (i32, [vp, vp, i64, i64, vp, vp, vp, vp, vp, sz, vp]),
             "exfold_calibrate_workspace_size": (sz, [vp, i64, i32]),
             "exfold_calibrate_projectors": (i32, [vp, vp, i64, dbl, dbl, i32, vp, vp, vp, vp, vp, sz, vp]),
+            "exfold_calibrate_diagonal": (i32, [vp, vp, i64, dbl, i32, vp, vp, vp, sz, vp]),
             "exfold_status_str": (ctypes.c_char_p, [i32]),
         }
         for name, (res, args) in sig.items():
@@ -269,11 +271,13 @@ def debug_buffers(layer: Layer, T: int, phase: str, budget: int, device) -> dict
 
 def moe_forward(layer: Layer, x, phase: str = "dense", budget: int = 0, S=None, L=None, h=None, y=None,
                 debug: dict | None = None, workspace=None, stream=None, events=None, static_tables=None,
-                safeguards: dict | None = None):
+                safeguards: dict | None = None, diag=None):
     """Folded MoE layer forward; returns y [T, d] (dtype of the layer).
 
     static_tables: (tgt, scl) from static_pool, for phase "decode_static".
     safeguards: prefill fold safeguards, keyword arguments of fold_opts.
+    diag: [N, N, d] diagonal maps from calibrate_diagonal, for phase "prefill_diag" (L is then the
+    diagonal loss table).
     events: optional ctypes array of N_EVENTS hipEvent_t handles recorded at the stage boundaries."""
     T = x.shape[0]
     _need(x, layer.dtype, (T, layer.d), "x")
@@ -282,8 +286,8 @@ def moe_forward(layer: Layer, x, phase: str = "dense", budget: int = 0, S=None, 
     ls = layer.struct()
     tgt, scl = static_tables if static_tables is not None else (None, None)
     cap, flags = fold_opts(**(safeguards or {}))
-    tb = _Tables(_ptr(S), _ptr(L), _ptr(h), _ptr(tgt), _ptr(scl), cap, flags) \
-        if (S is not None or tgt is not None) else None
+    tb = _Tables(_ptr(S), _ptr(L), _ptr(h), _ptr(tgt), _ptr(scl), cap, flags, _ptr(diag)) \
+        if (S is not None or L is not None or tgt is not None) else None
     dbg = None
     if debug is not None or events is not None:
         debug = debug or {}
@@ -332,3 +336,18 @@ def calibrate_projectors(layer: Layer, x_cal, lam: float = 1e-3, clip: float = 4
                                              _ptr(L), _ptr(h), _ptr(stats), _ptr(ws), ws.numel(), _stream(stream)),
            "exfold_calibrate_projectors")
     return (S, L, h, stats) if with_stats else (S, L, h)
+
+
+def calibrate_diagonal(layer: Layer, x_cal, lam: float = 1e-3, mode: str = "corouted", stream=None):
+    """Diagonal projector calibration; returns (Dg [N, N, d], Ld [N, N]) float32 device tensors."""
+    m = x_cal.shape[0]
+    N, d = layer.n_experts, layer.d
+    dev = x_cal.device
+    ls = layer.struct()
+    Dg = torch.empty((N, N, d), dtype=torch.float32, device=dev)
+    Ld = torch.empty((N, N), dtype=torch.float32, device=dev)
+    need = lib().exfold_calibrate_workspace_size(ctypes.byref(ls), m, CAL_MODE[mode])
+    ws = _workspace(need, dev)
+    _check(lib().exfold_calibrate_diagonal(ctypes.byref(ls), _ptr(x_cal), m, lam, CAL_MODE[mode], _ptr(Dg), _ptr(Ld),
+                                           _ptr(ws), ws.numel(), _stream(stream)), "exfold_calibrate_diagonal")
+    return Dg, Ld

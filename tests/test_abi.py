@@ -52,8 +52,8 @@ def ws_size(ly, T=64, phase=1, budget=1):
 
 
 def forward(ly, T=64, phase=1, budget=1, tables=True, ws_bytes=None, x=FAKE, y=FAKE, ws=FAKE * 16,
-            static=(FAKE, FAKE), flags=(0.0, 0)):
-    tb = X._Tables(FAKE, FAKE, FAKE, *static, *flags)
+            static=(FAKE, FAKE), flags=(0.0, 0), diag=FAKE):
+    tb = X._Tables(FAKE, FAKE, FAKE, *static, *flags, diag)
     if ws_bytes is None:
         ws_bytes = 0
     return X.lib().exfold_moe_forward(ctypes.byref(ly), ctypes.byref(tb) if tables else None, x, T, phase,
@@ -105,6 +105,11 @@ def test_forward_validation_codes():
     assert forward(ly, flags=(0.0, 16)) == X.ERR_ARG
     assert forward(ly, flags=(float("nan"), 1)) == X.ERR_ARG
     assert forward(ly, flags=(0.99, 7), ws_bytes=0) == X.ERR_WORKSPACE
+    # the diagonal phase needs the maps
+    assert forward(ly, phase=4, budget=1, diag=None) == X.ERR_NULL
+    assert forward(ly, phase=4, budget=0) == X.ERR_BUDGET
+    assert forward(ly, phase=4, budget=1, ws_bytes=0) == X.ERR_WORKSPACE
+    assert ws_size(ly, phase=4, budget=1) > ws_size(ly, phase=1, budget=1)
 
 
 def test_workspace_grows_with_tokens_and_budget():
@@ -155,6 +160,12 @@ def test_calibrate_validation():
     assert call(lam=-1.0) == X.ERR_ARG
     assert call(clip=float("nan")) == X.ERR_ARG
     assert call(S=None) == X.ERR_NULL
+    dcall = lambda **kw: L.exfold_calibrate_diagonal(ctypes.byref(ly), kw.get("x", f), 512, kw.get("lam", 1e-3),
+                                                     kw.get("mode", 0), kw.get("D", f), f, f * 16, 0, None)
+    assert dcall(mode=3) == X.ERR_ARG
+    assert dcall(lam=-1.0) == X.ERR_ARG
+    assert dcall(D=None) == X.ERR_NULL
+    assert dcall() == X.ERR_WORKSPACE
     assert call(x=None) == X.ERR_NULL
     assert call(ws=n - 1) == X.ERR_WORKSPACE
 
