@@ -293,6 +293,164 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
 }
 
 // ---------------------------------------------------------------------------
+// Skinny tile for decode (few rows per retained expert): 32 rows x 64 output
+// columns (gate/up: 32 gate + 32 up columns), BK = 128 per stage (256 contiguous
+// bytes of every weight row per load step), and the four waves split each
+// stage's reduction (wave w takes k16 steps w and w + 4) instead of the tile, so
+// the weights stream through many small workgroups (three per CU by LDS).  The
+// four partial tiles are added in wave order through LDS at the end.
+// ---------------------------------------------------------------------------
+constexpr int kSkM = 32, kSkN = 64, kSkK = 128;
+
+// LDS element offset of 16-byte chunk q of row r in a 256-byte row (16 chunks):
+// q XOR (r mod 16) spreads one chunk column of 16 consecutive rows over all banks.
+__device__ __forceinline__ int swz16(int r, int q) { return (r * 16 + (q ^ (r & 15))) * 8; }
+
+template <bool GATE_UP, bool DIRECT>
+__global__ __launch_bounds__(256) void expert_gemm_skinny(const GemmKArgs p) {
+  constexpr int PA = kSkM * 16 / 256, PB = kSkN * 16 / 256;  // 16-byte chunks per thread per stage
+  constexpr int STAGE = (kSkM + kSkN) * kSkK;                  // elements per LDS stage
+  __shared__ __attribute__((aligned(16))) bf16_t smem[2 * STAGE];
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+
+  TileId t;
+  if (!decode_tile(p, blockIdx.x, t)) return;
+  const int row0 = p.offsets[t.g] + t.mt * kSkM;
+  const int valid = min(kSkM, p.offsets[t.g + 1] - row0);
+  const bf16_t *Wg = (t.g < p.n_experts) ? p.W + (long long)t.g * p.w_stride : p.Ws;
+
+  // chunk c = i * 256 + tid: row c / 16, 16-byte column c % 16
+  const bf16_t *a_src[PA];
+  const bf16_t *b_src[PB];
+#pragma unroll
+  for (int i = 0; i < PA; ++i) {
+    const int c = i * 256 + tid, r = c >> 4;
+    const int rr = row0 + (r < valid ? r : 0);
+    const long long arow = GATE_UP ? (long long)p.row_token[rr] : (long long)rr;
+    a_src[i] = p.A + arow * p.lda + (long long)t.ks * p.kc + (c & 15) * 8;
+  }
+#pragma unroll
+  for (int i = 0; i < PB; ++i) {
+    const int c = i * 256 + tid, r = c >> 4;
+    int wrow;
+    if (GATE_UP)
+      wrow = (r < kSkN / 2) ? t.nt * (kSkN / 2) + r : p.inter + t.nt * (kSkN / 2) + (r - kSkN / 2);
+    else
+      wrow = t.nt * kSkN + r;
+    b_src[i] = Wg + (long long)wrow * p.ldw + (long long)t.ks * p.kc + (c & 15) * 8;
+  }
+
+  f32x16 acc[2];
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[j][r] = 0.f;
+
+#define EXF_SK_GLOAD(RA, RB, K0)                                                            \
+  do {                                                                                      \
+    _Pragma("unroll") for (int i_ = 0; i_ < PA; ++i_) RA[i_] =                              \
+        *reinterpret_cast<const u32x4 *>(a_src[i_] + (K0));                                 \
+    _Pragma("unroll") for (int i_ = 0; i_ < PB; ++i_) RB[i_] =                              \
+        *reinterpret_cast<const u32x4 *>(b_src[i_] + (K0));                                 \
+  } while (0)
+#define EXF_SK_LSTORE(RA, RB, BUF)                                                          \
+  do {                                                                                      \
+    bf16_t *As_ = smem + (BUF) * STAGE;                                                     \
+    bf16_t *Bs_ = As_ + kSkM * kSkK;                                                        \
+    _Pragma("unroll") for (int i_ = 0; i_ < PA; ++i_) {                                     \
+      const int c_ = i_ * 256 + tid;                                                        \
+      *reinterpret_cast<u32x4 *>(&As_[swz16(c_ >> 4, c_ & 15)]) = RA[i_];                   \
+    }                                                                                       \
+    _Pragma("unroll") for (int i_ = 0; i_ < PB; ++i_) {                                     \
+      const int c_ = i_ * 256 + tid;                                                        \
+      *reinterpret_cast<u32x4 *>(&Bs_[swz16(c_ >> 4, c_ & 15)]) = RB[i_];                   \
+    }                                                                                       \
+  } while (0)
+  // wave w: k16 steps w and w + 4 of the stage; lane l reads row l % 32, 8 k at (l / 32) * 8
+#define EXF_SK_COMPUTE(BUF)                                                                 \
+  do {                                                                                      \
+    const bf16_t *As_ = smem + (BUF) * STAGE;                                               \
+    const bf16_t *Bs_ = As_ + kSkM * kSkK;                                                  \
+    _Pragma("unroll") for (int h_ = 0; h_ < 2; ++h_) {                                      \
+      const int ch_ = (wave + 4 * h_) * 2 + (lane >> 5);                                    \
+      const bf16x8 a_ = *reinterpret_cast<const bf16x8 *>(&As_[swz16(lane & 31, ch_)]);     \
+      const bf16x8 b0_ = *reinterpret_cast<const bf16x8 *>(&Bs_[swz16(lane & 31, ch_)]);    \
+      const bf16x8 b1_ = *reinterpret_cast<const bf16x8 *>(&Bs_[swz16(32 + (lane & 31), ch_)]); \
+      acc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_, b0_, acc[0], 0, 0, 0);           \
+      acc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a_, b1_, acc[1], 0, 0, 0);           \
+    }                                                                                       \
+  } while (0)
+
+  // Two register sets: the loads of stage kt + 2 fly during the MFMAs of stage kt.
+  const int KT = p.kc / kSkK;
+  const int k_last = (KT - 1) * kSkK;
+  u32x4 ra0[PA], rb0[PB], ra1[PA], rb1[PB];
+  EXF_SK_GLOAD(ra0, rb0, 0);
+  EXF_SK_LSTORE(ra0, rb0, 0);
+  EXF_SK_GLOAD(ra1, rb1, min(kSkK, k_last));
+  __syncthreads();
+  int kt = 0;
+  for (; kt + 2 <= KT; kt += 2) {
+    EXF_SK_GLOAD(ra0, rb0, min((kt + 2) * kSkK, k_last));
+    EXF_SK_COMPUTE(0);
+    EXF_SK_LSTORE(ra1, rb1, 1);
+    __syncthreads();
+    EXF_SK_GLOAD(ra1, rb1, min((kt + 3) * kSkK, k_last));
+    EXF_SK_COMPUTE(1);
+    EXF_SK_LSTORE(ra0, rb0, 0);
+    __syncthreads();
+  }
+  if (kt < KT) EXF_SK_COMPUTE(0);
+#undef EXF_SK_GLOAD
+#undef EXF_SK_LSTORE
+#undef EXF_SK_COMPUTE
+
+  // Partial tiles of the four waves, added in wave order (LDS reused).
+  __syncthreads();
+  float *red = reinterpret_cast<float *>(smem);  // [4][2][16][64] floats = 32 KB
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) red[((wave * 2 + j) * 16 + r) * 64 + lane] = acc[j][r];
+  __syncthreads();
+  // wave w finishes accumulator registers r in [4 w, 4 w + 4) of both column halves
+#pragma unroll
+  for (int j = 0; j < 2; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int r = wave * 4 + q;
+      float v = red[((0 * 2 + j) * 16 + r) * 64 + lane];
+#pragma unroll
+      for (int w = 1; w < 4; ++w) v += red[((w * 2 + j) * 16 + r) * 64 + lane];
+      acc[j][q] = v;
+    }
+
+  // ---- epilogue: rows (r / 4) * 8 + (lane / 32) * 4 + r % 4 of the 32x32 MFMA layout ----
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int r = wave * 4 + q;
+    const int ml = (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+    if (ml < valid) {
+      const int row = row0 + ml;
+      if (GATE_UP) {
+        const int n = t.nt * (kSkN / 2) + (lane & 31);
+        p.H[(long long)row * p.inter + n] = f32_to_bf16(silu(acc[0][q]) * acc[1][q]);
+      } else {
+        const float w = p.row_w[row];
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          const int n = t.nt * kSkN + j * 32 + (lane & 31);
+          if (DIRECT)
+            p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(acc[j][q] * w);
+          else
+            p.Y[((long long)t.ks * p.rows + row) * p.d + n] = acc[j][q] * w;
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // float32 path (SIMT, one thread per output element): the fp32 layer is small.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ int find_group(const int32_t *offsets, int groups, int row) {
@@ -370,36 +528,38 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
     *dn = GemmPlan{4, 64, 1, 0, kGemmSimt};
     return;
   }
-  // 128x128 tiles everywhere; the plan depends on the problem only (rows, groups,
-  // sizes), never on the phase, so equal problems get equal plans.
-  *gu = GemmPlan{128, 128, 1, 0, kGemmTile};
-  *dn = GemmPlan{128, 128, 1, 0, kGemmTile};
-  const int mt_max = rows / 128 + groups;  // >= sum over groups of ceil(rows_g / 128)
-  gu->grid = mt_max * (inter / 64);
-  // Few expected tiles (few rows per retained expert): split the down projection's
-  // reduction so the workgroups still cover every CU.  Partial sums land in
-  // separate buffers and are added in a fixed order by the combine.
+  // The plan depends on the problem only (rows, groups, sizes), never on the
+  // phase, so equal problems get equal plans.
   const int active = active_groups < 1 ? 1 : active_groups;
-  const int mt_expect = (rows + 127) / 128 > active ? (rows + 127) / 128 : active;
-  const int dn_tiles = mt_expect * (d / 128);
-  if (dn_tiles < 2 * cu_count) {
-    const int want = (2 * cu_count + dn_tiles - 1) / dn_tiles;
-    dn->ksplit = largest_divisor_at_most(inter / kBK, want > 8 ? 8 : want);
+  // Few rows per retained expert (decode): skinny 32x64 tiles stream the weights
+  // through many small workgroups; otherwise 128x128 tiles.  The gate/up
+  // projection keeps 128-row tiles once the experts hold more than about 24
+  // rows each and those tiles already cover the CUs: skinny tiles then read the
+  // weights of a busy expert more than once.
+  const bool sk_shapes = inter % 128 == 0 && d % 64 == 0;
+  const int mt128 = (rows + 127) / 128 > active ? (rows + 127) / 128 : active;
+  const bool gu_skinny = sk_shapes && (rows <= 24 * active || mt128 * (inter / 64) < cu_count);
+  const bool dn_skinny = sk_shapes && rows <= 64 * active;
+  if (gu_skinny) {
+    *gu = GemmPlan{kSkM, kSkN, 1, 0, kGemmSkinny};
+    gu->grid = (rows / kSkM + groups) * (inter / (kSkN / 2));  // >= sum of ceil(rows_g / 32) tiles
+  } else {
+    *gu = GemmPlan{128, 128, 1, 0, kGemmTile};
+    gu->grid = (rows / 128 + groups) * (inter / 64);
   }
-  dn->grid = mt_max * (d / 128) * dn->ksplit;
-}
-
-template <int BM, int BN, int STAGES>
-static void launch_tile(const GemmKArgs &ga, const GemmKArgs &da, int gu_grid, int dn_grid,
-                        bool direct, hipStream_t s, hipEvent_t ev_mid) {
-  if (gu_grid > 0) expert_gemm_tile<BM, BN, STAGES, true, false><<<gu_grid, 256, 0, s>>>(ga);
-  if (ev_mid) (void)hipEventRecord(ev_mid, s);
-  if (dn_grid > 0) {
-    if (direct)
-      expert_gemm_tile<BM, BN, STAGES, false, true><<<dn_grid, 256, 0, s>>>(da);
-    else
-      expert_gemm_tile<BM, BN, STAGES, false, false><<<dn_grid, 256, 0, s>>>(da);
+  // Few expected tiles: split the down projection's reduction so the workgroups
+  // still cover every CU.  Partial sums land in separate buffers and are added
+  // in a fixed order by the combine.
+  const int bm = dn_skinny ? kSkM : 128, bn = dn_skinny ? kSkN : 128;
+  const int kk = dn_skinny ? kSkK : kBK, fill = dn_skinny ? 3 : 2;
+  *dn = GemmPlan{bm, bn, 1, 0, dn_skinny ? kGemmSkinny : kGemmTile};
+  const int mt_expect = (rows + bm - 1) / bm > active ? (rows + bm - 1) / bm : active;
+  const int dn_tiles = mt_expect * (d / bn);
+  if (dn_tiles < fill * cu_count) {
+    const int want = (fill * cu_count + dn_tiles - 1) / dn_tiles;
+    dn->ksplit = largest_divisor_at_most(inter / kk, want > 8 ? 8 : want);
   }
+  dn->grid = (rows / bm + groups) * (d / bn) * dn->ksplit;
 }
 
 hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const GemmPlan &dn,
@@ -461,7 +621,26 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
   da.y = static_cast<bf16_t *>(a.y);
   da.row_w = a.row_w;
 
-  launch_tile<128, 128, 2>(ga, da, gu.grid, dn.grid, a.direct, s, ev_mid);
+  if (gu.grid > 0) {
+    if (gu.kind == kGemmSkinny)
+      expert_gemm_skinny<true, false><<<gu.grid, 256, 0, s>>>(ga);
+    else
+      expert_gemm_tile<128, 128, 2, true, false><<<gu.grid, 256, 0, s>>>(ga);
+  }
+  if (ev_mid) (void)hipEventRecord(ev_mid, s);
+  if (dn.grid > 0) {
+    if (dn.kind == kGemmSkinny) {
+      if (a.direct)
+        expert_gemm_skinny<false, true><<<dn.grid, 256, 0, s>>>(da);
+      else
+        expert_gemm_skinny<false, false><<<dn.grid, 256, 0, s>>>(da);
+    } else {
+      if (a.direct)
+        expert_gemm_tile<128, 128, 2, false, true><<<dn.grid, 256, 0, s>>>(da);
+      else
+        expert_gemm_tile<128, 128, 2, false, false><<<dn.grid, 256, 0, s>>>(da);
+    }
+  }
   return hipGetLastError();
 }
 

@@ -66,12 +66,13 @@ hipError_t launch_static_pool(const float *h, int N, int D, const float *S, cons
                               hipStream_t s);
 
 // ---- expert GEMMs and combine (k_gemm.hip) ----
-enum { kGemmSimt = 0, kGemmTile = 1 };
+// kGemmTile: 128x128 tiles; kGemmSkinny: 32x64 tiles for few rows per expert.
+enum { kGemmSimt = 0, kGemmTile = 1, kGemmSkinny = 2 };
 struct GemmPlan {
   int bm, bn;  // tile height (rows) and width (output columns, or weight rows for gate/up)
   int ksplit;  // splits of the reduction (down projection only; partial outputs)
   int grid;    // workgroups launched (an upper bound on the device-side tile count)
-  int kind;    // kGemmSimt (float32 layers) or kGemmTile (bf16 MFMA tiles)
+  int kind;    // kGemmSimt (float32 layers), kGemmTile or kGemmSkinny (bf16 MFMA tiles)
 };
 struct ExpertArgs {
   int dtype;
