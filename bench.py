@@ -12,7 +12,10 @@ stand-ins (their values only steer selection, not the amount of work).
 Prints ONE JSON line: value = prefill TFLOP/s (algorithmic flops / mean
 prefill-layer time), with the decode layer's us/layer and HBM GB/s, the
 roofline of the dominant kernel (the prefill gate/up GEMM, timed live with
-HIP events on its stream) and the CPU oracle timed on a bounded sample.
+HIP events on its stream) and the CPU oracle timed on a bounded sample.  The
+timed steps record HIP events only at the layer boundaries and around the
+dominant kernel; the per-stage breakdown in the line comes from a second,
+fully instrumented run of the same steps after the timed region.
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload mixtral|qwen3|glm|qwen3-decode]
 
@@ -151,8 +154,8 @@ def decode_bytes(shape, B, touched):
     return w + shape.n_experts * shape.d * esz + 2 * B * shape.d * esz + B * shape.top_k * 16
 
 
-def run_phase(X, layer, x, phase, budget, tables, steps, warmup, ev, stream, dbg=None):
-    """Warm up, then time `steps` forwards; returns per-step stage durations (ms)."""
+def run_phase(X, layer, x, phase, budget, tables, warmup, dbg=None):
+    """Output and workspace of one phase, after `warmup` untimed forwards."""
     import torch
     S, L, h = tables
     y = torch.empty_like(x)
@@ -160,8 +163,7 @@ def run_phase(X, layer, x, phase, budget, tables, steps, warmup, ev, stream, dbg
     for _ in range(warmup):
         X.moe_forward(layer, x, phase, budget, S, L, h, y=y, workspace=ws, debug=dbg)
     torch.cuda.synchronize()
-    arrs = [ev.array(X.N_EVENTS) for _ in range(steps)]
-    return y, ws, arrs
+    return y, ws
 
 
 def main():
@@ -239,8 +241,25 @@ def main():
     ev = HipEvents()
     dbg_d = {"pool_size": torch.empty(1, dtype=torch.int32, device="cuda")}
     S, L, h = tables
-    y_p, ws_p, ev_p = run_phase(X, layer, x_p, "prefill", kp, tables, args.steps, args.warmup, ev, stream)
-    y_d, ws_d, ev_d = run_phase(X, layer, x_d, "decode", D, tables, args.steps, args.warmup, ev, stream, dbg_d)
+    y_p, ws_p = run_phase(X, layer, x_p, "prefill", kp, tables, args.warmup)
+    y_d, ws_d = run_phase(X, layer, x_d, "decode", D, tables, args.warmup, dbg_d)
+    names = X.EVENT_NAMES
+    START, PERMUTE, GATE_UP, END = (names.index(n) for n in ("start", "permute", "gate_up", "end"))
+
+    def sparse(idx):
+        """Per-step event arrays that record only the stage boundaries in idx (NULL entries are skipped)."""
+        out = []
+        for _ in range(args.steps):
+            full = ev.array(X.N_EVENTS)
+            arr = (ctypes.c_void_p * X.N_EVENTS)()
+            for i in idx:
+                arr[i] = full[i]
+            out.append(arr)
+        return out
+
+    # timed steps: the layer boundaries, plus the gate/up GEMM launch of the prefill forward (the
+    # dominant kernel); no other events inside the layer
+    ev_p, ev_d = sparse((START, PERMUTE, GATE_UP, END)), sparse((START, END))
     edge = ev.array(2)
     torch.cuda.synchronize()
     # ---- timed region: exactly `steps` steps, synchronised on both sides ----
@@ -251,23 +270,35 @@ def main():
     ev.record(edge[1], sptr)
     torch.cuda.synchronize()
     total_ms = ev.ms(edge[0], edge[1])
-    names = X.EVENT_NAMES
+
+    def mean_us(arrs, a, b):
+        return float(np.mean([ev.ms(x[a], x[b]) for x in arrs])) * 1e3
+
+    layer_p, layer_d = mean_us(ev_p, START, END), mean_us(ev_d, START, END)
+    gate_up_us = mean_us(ev_p, PERMUTE, GATE_UP)
+
+    # stage breakdown (informational): a separate run with an event at every stage boundary
+    st_ev_p, st_ev_d = [ev.array(X.N_EVENTS) for _ in range(args.steps)], [ev.array(X.N_EVENTS) for _ in range(args.steps)]
+    for k in range(args.steps):
+        X.moe_forward(layer, x_p, "prefill", kp, S, L, h, y=y_p, workspace=ws_p, events=st_ev_p[k])
+        X.moe_forward(layer, x_d, "decode", D, S, L, h, y=y_d, workspace=ws_d, events=st_ev_d[k], debug=dbg_d)
+    torch.cuda.synchronize()
 
     def stages(arrs):
         out = {}
         for i in range(1, len(names)):
-            out[names[i]] = float(np.mean([ev.ms(a[i - 1], a[i]) for a in arrs])) * 1e3
-        out["layer"] = float(np.mean([ev.ms(a[0], a[len(names) - 1]) for a in arrs])) * 1e3
+            out[names[i]] = mean_us(arrs, i - 1, i)
+        out["layer"] = mean_us(arrs, 0, len(names) - 1)
         return out
 
-    st_p, st_d = stages(ev_p), stages(ev_d)
+    st_p, st_d = stages(st_ev_p), stages(st_ev_d)
     touched = int(dbg_d["pool_size"].item())
     flops_p = prefill_flops(shape, T, kp)
-    tflops = flops_p / (st_p["layer"] * 1e-6) / 1e12
+    tflops = flops_p / (layer_p * 1e-6) / 1e12
     gu_flops = 4 * shape.d * shape.inter * (T * kp + (T if shape.shared_inter else 0))
-    gu_tflops = gu_flops / (st_p["gate_up"] * 1e-6) / 1e12
+    gu_tflops = gu_flops / (gate_up_us * 1e-6) / 1e12
     bytes_d = decode_bytes(shape, B, touched)
-    gbs_d = bytes_d / (st_d["layer"] * 1e-6) / 1e9
+    gbs_d = bytes_d / (layer_d * 1e-6) / 1e9
     log(f"prefill stages (us): {json.dumps({k: round(v, 1) for k, v in st_p.items()})}")
     log(f"decode stages (us): {json.dumps({k: round(v, 1) for k, v in st_d.items()})}")
 
@@ -297,19 +328,21 @@ def main():
         "dtype": "bf16",
         "data": "synthetic (seeded N(0,1) tokens, N(0,0.02^2) weights, seeded stand-in projector tables)",
         "config": {"workload": workload, "prefill_tokens": T, "k_pre": kp, "decode_tokens": B, "pool_budget": D},
-        "prefill": {"us_per_layer": round(st_p["layer"], 1), "tflops": round(tflops, 2),
+        "prefill": {"us_per_layer": round(layer_p, 1), "tflops": round(tflops, 2),
                     "frac_mfma_peak": round(tflops / PEAK_BF16_TFLOPS, 4),
-                    "algorithmic_gflop": round(flops_p / 1e9, 2), "stages_us": {k: round(v, 1) for k, v in st_p.items()}},
-        "decode": {"us_per_layer": round(st_d["layer"], 1), "hbm_gbs": round(gbs_d, 1),
+                    "algorithmic_gflop": round(flops_p / 1e9, 2),
+                    "stages_us_instrumented": {k: round(v, 1) for k, v in st_p.items()}},
+        "decode": {"us_per_layer": round(layer_d, 1), "hbm_gbs": round(gbs_d, 1),
                    "frac_hbm_peak": round(gbs_d / PEAK_HBM_GBS, 4), "experts_touched": touched,
-                   "algorithmic_mb": round(bytes_d / 1e6, 2), "stages_us": {k: round(v, 1) for k, v in st_d.items()}},
+                   "algorithmic_mb": round(bytes_d / 1e6, 2),
+                   "stages_us_instrumented": {k: round(v, 1) for k, v in st_d.items()}},
         "roofline": {"bound": "mfma", "achieved": round(gu_tflops, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4),
                      "traffic": None if traffic is None else traffic["bytes_per_launch"],
                      "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "algorithmic_bytes": gu_bytes,
                      "kernel": DOMINANT + " (prefill gate/up GEMM, fused SiLU*up)",
-                     "per_launch_gflop": round(gu_flops / 1e9, 2), "avg_launch_us": round(st_p["gate_up"], 1)},
+                     "per_launch_gflop": round(gu_flops / 1e9, 2), "avg_launch_us": round(gate_up_us, 1)},
         "cpu_baseline": cpu,
     }
     ev.close()
@@ -384,8 +417,9 @@ def _find(dirname, suffix):
 
 
 def prof_summary(d, workload, steps):
-    """Markdown summary of the rocprofv3 runs under d; `steps` is the --steps of the traced run, whose
-    last `steps` launches of each kernel are the timed ones."""
+    """Markdown summary of the rocprofv3 runs under d; `steps` is the --steps of the traced run.  Each
+    kernel's launches end with the `steps` timed steps and then the `steps` steps of the instrumented
+    stage breakdown, so the timed launches are the `steps` before the last `steps`."""
     mean = lambda v: sum(v) / len(v)
     cf = _counters(_find(os.path.join(d, "copyfetch"), "counter_collection.csv"))
     cw = _counters(_find(os.path.join(d, "copywrite"), "counter_collection.csv"))
@@ -416,7 +450,7 @@ def prof_summary(d, workload, steps):
         rd = mean(fe[key]["FETCH_SIZE"]) * 1024 * f_fac if key in fe else None
         wt = mean(wr[key]["WRITE_SIZE"]) * 1024 * w_fac if key in wr else None
         fmt = lambda b: "-" if b is None else f"{b / 1e6:.1f}"
-        timed = mean(v[-steps:]) if len(v) >= steps else mean(v)
+        timed = mean(v[-2 * steps:-steps]) if len(v) >= 2 * steps else mean(v)
         lines.append(f"| `{name[:80]}` | {key[1]} | {len(v)} | {mean(v):.1f} | {timed:.1f} | {min(v):.1f} | "
                      f"{fmt(rd)} | {fmt(wt)} |")
         if record is None and DOMINANT in key[0] and rd is not None and wt is not None:

@@ -148,7 +148,8 @@ enum {
  * as the buffer of that intermediate (no extra copy); NULL members live in the
  * workspace.  Sizes: K_out = min(K', K) in prefill, K otherwise.
  * `events`, if non-NULL, holds EXFOLD_N_EVENTS hipEvent_t handles (created by
- * the caller) that are recorded on the stream at the stage boundaries above. */
+ * the caller) that are recorded on the stream at the stage boundaries above;
+ * a NULL entry is skipped (no event at that boundary). */
 typedef struct exfold_debug {
   float *logits;        /* [T, N]      router logits                                   */
   int32_t *topk_ids;    /* [T, K]      Top-K expert ids                                */
