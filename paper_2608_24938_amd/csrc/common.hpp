@@ -2,6 +2,7 @@
 #pragma once
 
 #include <hip/hip_runtime.h>
+#include <type_traits>
 #include <stdint.h>
 
 #include "exfold.h"
@@ -48,26 +49,67 @@ __device__ __forceinline__ uint32_t float_key(float v) {
 
 __device__ __forceinline__ int clamp_id(int e, int n) { return e < 0 ? 0 : (e >= n ? n - 1 : e); }
 
-__device__ __forceinline__ uint64_t shfl_xor_u64(uint64_t v, int mask) {
-  uint32_t lo = __shfl_xor((unsigned)(v & 0xffffffffu), mask, kWave);
-  uint32_t hi = __shfl_xor((unsigned)(v >> 32), mask, kWave);
+// Cross-lane helpers built on DPP (in-register, within rows of 16 lanes) and
+// readlane (whole wave, uniform lane index) instead of LDS permutes, whose
+// latency chains dominated the one-wave reductions.  All take full waves.
+// DPP controls: quad_perm [1,0,3,2] and [2,3,0,1], row_half_mirror, row_mirror.
+template <int CTRL>
+__device__ __forceinline__ uint32_t dpp_u32(uint32_t v, uint32_t old) {
+  return (uint32_t)__builtin_amdgcn_update_dpp((int)old, (int)v, CTRL, 0xf, 0xf, false);
+}
+template <int CTRL>
+__device__ __forceinline__ uint64_t dpp_u64(uint64_t v, uint64_t old) {
+  const uint32_t lo = dpp_u32<CTRL>((uint32_t)v, (uint32_t)old);
+  const uint32_t hi = dpp_u32<CTRL>((uint32_t)(v >> 32), (uint32_t)(old >> 32));
   return (uint64_t(hi) << 32) | lo;
 }
-
-__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) {
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) {
-    uint64_t o = shfl_xor_u64(v, m);
-    v = o > v ? o : v;
-  }
-  return v;
+__device__ __forceinline__ uint32_t readlane_u32(uint32_t v, int lane) {
+  return (uint32_t)__builtin_amdgcn_readlane((int)v, lane);
+}
+__device__ __forceinline__ uint64_t readlane_u64(uint64_t v, int lane) {
+  return (uint64_t(readlane_u32((uint32_t)(v >> 32), lane)) << 32) | readlane_u32((uint32_t)v, lane);
+}
+__device__ __forceinline__ double readlane_f64(double v, int lane) {
+  return __longlong_as_double((long long)readlane_u64((uint64_t)__double_as_longlong(v), lane));
+}
+__device__ __forceinline__ float readlane_f32(float v, int lane) {
+  return __uint_as_float(readlane_u32(__float_as_uint(v), lane));
 }
 
-__device__ __forceinline__ double shfl_f64(double v, int src) {
-  int64_t b = __double_as_longlong(v);
-  int lo = __shfl((int)(b & 0xffffffff), src, kWave);
-  int hi = __shfl((int)(b >> 32), src, kWave);
-  return __longlong_as_double((int64_t(uint32_t(hi)) << 32) | uint32_t(lo));
+// Max (MAX) or min of a 64-bit key over the wave; every lane gets the result.
+template <bool MAX>
+__device__ __forceinline__ uint64_t wave_reduce_u64(uint64_t v) {
+  auto pick = [](uint64_t a, uint64_t b) { return MAX ? (a > b ? a : b) : (a < b ? a : b); };
+  v = pick(v, dpp_u64<0xB1>(v, v));
+  v = pick(v, dpp_u64<0x4E>(v, v));
+  v = pick(v, dpp_u64<0x141>(v, v));
+  v = pick(v, dpp_u64<0x140>(v, v));
+  return pick(pick(readlane_u64(v, 0), readlane_u64(v, 16)), pick(readlane_u64(v, 32), readlane_u64(v, 48)));
+}
+__device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) { return wave_reduce_u64<true>(v); }
+__device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) { return wave_reduce_u64<false>(v); }
+
+// Sum over the wave in a fixed association (pairs within quads, half-rows,
+// rows, then the four rows in order); every lane gets the same value.
+__device__ __forceinline__ double wave_sum_f64(double v) {
+  auto step = [](double x, auto ctrl) {
+    const uint64_t b = (uint64_t)__double_as_longlong(x);
+    return x + __longlong_as_double((long long)dpp_u64<decltype(ctrl)::value>(b, 0ull));
+  };
+  v = step(v, std::integral_constant<int, 0xB1>{});
+  v = step(v, std::integral_constant<int, 0x4E>{});
+  v = step(v, std::integral_constant<int, 0x141>{});
+  v = step(v, std::integral_constant<int, 0x140>{});
+  return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
+}
+
+// Workgroup barrier that orders LDS accesses only: global stores issued before
+// it are not waited for.  For kernels whose threads exchange data through LDS
+// alone and whose global outputs are read only after the kernel.
+__device__ __forceinline__ void lds_barrier() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (lane == 0) ? 0ull : (~0ull >> (64 - lane)); }

@@ -213,11 +213,9 @@ __device__ __forceinline__ void wave_topk_softmax(const float v[4], int N, int K
   const float c0 = __shfl(v[0], src, kWave), c1 = __shfl(v[1], src, kWave);
   const float c2 = __shfl(v[2], src, kWave), c3 = __shfl(v[3], src, kWave);
   const double r = (double)(reg == 0 ? c0 : reg == 1 ? c1 : reg == 2 ? c2 : c3);
-  const double r0 = shfl_f64(r, 0);  // route 0 holds the largest logit
-  double z = (lane < K) ? exp(r - r0) : 0.0;
-  double sum = z;
-#pragma unroll
-  for (int m = 32; m >= 1; m >>= 1) sum += __shfl_xor(sum, m, kWave);
+  const double r0 = readlane_f64(r, 0);  // route 0 holds the largest logit
+  const double z = (lane < K) ? exp(r - r0) : 0.0;
+  const double sum = wave_sum_f64(z);
   my_w = (float)(z / sum);
 }
 
@@ -256,7 +254,7 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
     const double score = (lane < K) ? (double)my_w * (double)h[my_id] : 0.0;
     int rank = 0;
     for (int j = 0; j < K; ++j) {
-      const double sj = shfl_f64(score, j);
+      const double sj = readlane_f64(score, j);
       rank += (j != lane) && (sj > score || (sj == score && j < lane));
     }
     kept = (lane < K) && rank < k_pre;
@@ -268,7 +266,7 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   const uint64_t kmask = __ballot(kept);
   int ids[kMaxTopK];
 #pragma unroll
-  for (int j = 0; j < kMaxTopK; ++j) ids[j] = __shfl(my_id, j < K ? j : 0, kWave);
+  for (int j = 0; j < kMaxTopK; ++j) ids[j] = (int)readlane_u32((uint32_t)my_id, j < K ? j : 0);
 
   // Omitted route: first minimum of L[s, t] over the retained routes in route
   // order (with the loss cap: over those with L[s, t] <= cap; none -> dropped).
@@ -323,13 +321,13 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   double w_ret = 0.0;
   if (conf)
     for (int j = 0; j < K; ++j)
-      if ((kmask >> j) & 1ull) w_ret = __dadd_rn(w_ret, (double)__shfl(my_w, j, kWave));
+      if ((kmask >> j) & 1ull) w_ret = __dadd_rn(w_ret, (double)readlane_f32(my_w, j));
   const double share = (conf && kept) ? __ddiv_rn((double)my_w, w_ret) : 0.0;
   double acc = (double)my_w;
   for (int j = 0; j < K; ++j) {
-    const int tl = __shfl(tgt_lane, j, kWave);
-    const double c = shfl_f64(contrib, j);
-    const double r = shfl_f64(rest, j);
+    const int tl = (int)readlane_u32((uint32_t)tgt_lane, j);
+    const double c = readlane_f64(contrib, j);
+    const double r = readlane_f64(rest, j);
     if (tl == lane) acc = __dadd_rn(acc, c);
     if (conf && tl >= 0 && kept) acc = __dadd_rn(acc, __dmul_rn(r, share));
   }
@@ -337,8 +335,8 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   if (flags & EXFOLD_FOLD_RENORM) {
     double w_all = 0.0, tot = 0.0;
     for (int j = 0; j < K; ++j) {
-      w_all = __dadd_rn(w_all, (double)__shfl(my_w, j, kWave));
-      const double a = shfl_f64(acc, j);
+      w_all = __dadd_rn(w_all, (double)readlane_f32(my_w, j));
+      const double a = readlane_f64(acc, j);
       if ((kmask >> j) & 1ull) tot = __dadd_rn(tot, a);
     }
     if (tot > 0.0) acc = __dmul_rn(acc, __ddiv_rn(w_all, tot));
@@ -473,68 +471,70 @@ __global__ __launch_bounds__(kPoolThreads) void decode_pool_fold_kernel(
 // Per-source tables of a decode pool (Eq. minimum_loss_assignment over the
 // pool): a source in the pool maps to itself with scale 1, any other source to
 // the first minimum of L[s, t] over the pool in pool order, with scale S[s, t].
-// Wave w takes sources w + 16 u; lane l reads L[s, pool[l + 64 c]] and
-// S[s, pool[l + 64 c]] (eight sources per batch, so 16 loads are in flight)
-// and the wave keeps the first minimum (64-bit key: value, index) with its
-// scale.  pool/in_pool/n_pool in LDS; writes tgt/scl (LDS) and tgt_g/scl_g.
+// Thread (s, p) = (tid / P, tid % P) reads L and S at the pool members
+// p, p + P, ... (P = threads per source, all its loads in flight together) and
+// keeps its first minimum as a 64-bit key (value, pool position); an LDS
+// atomic min per source combines the threads, and the one thread whose key won
+// writes the target and its scale.  Called by the whole workgroup (it holds
+// two barriers); pool/in_pool/n_pool in LDS; writes tgt/scl (LDS) and
+// tgt_g/scl_g (either may be NULL).
 __device__ void pool_tables(int N, const float *__restrict__ S, const float *__restrict__ L,
                             const int *pool, const int *in_pool, int n_pool, int *tgt, float *scl,
                             int32_t *__restrict__ tgt_g, float *__restrict__ scl_g) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  constexpr int kWaves = kPoolThreads / kWave;
-  for (int base = wave; base < N; base += kWaves * 8) {
-    uint64_t best[8];
-    float bs[8];
+  constexpr int kBatch = 8;  // loads in flight per thread
+  __shared__ unsigned long long best[kMaxExperts];
+  const int tid = threadIdx.x;
+  const int P = kPoolThreads / N;  // N <= kMaxExperts <= kPoolThreads / 4
+  // the P threads of one source are adjacent, so a wave's loads stay within a
+  // few rows of L and S (few cache lines per load instruction)
+  const int src = tid / P, part = tid % P;
+  const bool mine = src < N;
+  if (tid < N) best[tid] = ~0ull;
+  __syncthreads();
+  uint64_t key = ~0ull;
+  float s_key = 1.0f;
+  if (mine && !in_pool[src]) {
+    const float *lrow = L + (size_t)src * N, *srow = S + (size_t)src * N;
+    for (int j0 = part; j0 < n_pool; j0 += kBatch * P) {
+      float lv[kBatch], sv[kBatch];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      best[u] = ~0ull;
-      bs[u] = 1.0f;
-    }
-    for (int c = 0; c < n_pool; c += kWave) {
-      const int j = c + lane;
-      const bool live = j < n_pool;
-      const int pj = live ? pool[j] : 0;
-      float lv[8], sv[8];
-#pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const size_t o = (size_t)min(base + kWaves * u, N - 1) * N + pj;
-        lv[u] = L[o];
-        sv[u] = S[o];
+      for (int b = 0; b < kBatch; ++b) {
+        const int j = j0 + b * P;
+        lv[b] = 0.f;
+        sv[b] = 0.f;
+        if (j < n_pool) {
+          const int t = pool[j];
+          lv[b] = lrow[t];
+          sv[b] = srow[t];
+        }
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
-        const uint64_t key = live ? ((uint64_t(float_key(lv[u])) << 32) | uint64_t(j)) : ~0ull;
-        if (key < best[u]) {
-          best[u] = key;
-          bs[u] = sv[u];
+      for (int b = 0; b < kBatch; ++b) {
+        const int j = j0 + b * P;
+        const uint64_t k = (uint64_t(float_key(lv[b])) << 32) | uint64_t(uint32_t(j));
+        if (j < n_pool && k < key) {
+          key = k;
+          s_key = sv[b];
         }
       }
     }
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int src = base + kWaves * u;
-      uint64_t b = best[u];
-#pragma unroll
-      for (int m = 32; m >= 1; m >>= 1) {
-        const uint64_t o = shfl_xor_u64(b, m);
-        b = o < b ? o : b;
-      }
-      // the lane holding the minimum (keys are distinct: they carry the index)
-      const uint64_t holder = __ballot(best[u] == b);
-      const float s_min = __shfl(bs[u], holder ? (int)__ffsll((long long)holder) - 1 : 0, kWave);
-      if (src < N && lane == 0) {
-        int t_best = src;
-        float s_best = 1.0f;
-        if (!in_pool[src] && n_pool > 0) {
-          t_best = pool[(int)(b & 0xffffffffu)];
-          s_best = s_min;
-        }
-        tgt[src] = t_best;
-        scl[src] = s_best;
-        if (tgt_g) tgt_g[src] = t_best;
-        if (scl_g) scl_g[src] = s_best;
-      }
-    }
+    if (key != ~0ull) atomicMin(&best[src], (unsigned long long)key);
+  }
+  __syncthreads();
+  if (!mine) return;
+  int t_out = -1;
+  float s_out = 1.0f;
+  if (in_pool[src] || n_pool == 0) {
+    if (part == 0) t_out = src;  // maps to itself
+  } else if (key != ~0ull && key == best[src]) {
+    t_out = pool[(int)(key & 0xffffffffu)];
+    s_out = s_key;
+  }
+  if (t_out >= 0) {
+    tgt[src] = t_out;
+    scl[src] = s_out;
+    if (tgt_g) tgt_g[src] = t_out;
+    if (scl_g) scl_g[src] = s_out;
   }
 }
 
@@ -635,6 +635,8 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   __shared__ int cur[kMaxExperts];
   __shared__ int wcnt[kFrontWaves][kMaxExperts];
   __shared__ int n_pool;
+  // Threads hand data to each other through LDS only, and no global output is
+  // read back here, so the phase barriers order LDS alone.
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int slots = B * K;
   const int dcap = min(D, N);
@@ -656,7 +658,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
       in_pool[tid] = te == tid;
     }
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- pool (Eq. decode_budget): exact fixed-point weight sums ----
   for (int j = tid; j < slots; j += kPoolThreads) {
@@ -670,7 +672,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
       atomicAdd(&cnt[e], 1);
     }
   }
-  __syncthreads();
+  lds_barrier();
   if (dynamic) {
   if (tid < N) score[tid] = (double)(long long)wsum[tid] * (double)h_e;
   const int n_cand = __syncthreads_count(tid < N && cnt[tid] > 0);
@@ -690,20 +692,20 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
       atomicAdd(&rank_sh[e], my);
     }
   }
-  __syncthreads();
+  lds_barrier();
   if (tid < N && cnt[tid] > 0 && rank_sh[tid] < dcap) {
     pool[rank_sh[tid]] = tid;
     in_pool[tid] = 1;
   }
   if (tid == 0) n_pool = min(dcap, n_cand);
-  __syncthreads();
+  lds_barrier();
   if (tid < dcap) pool_g[tid] = (tid < n_pool) ? pool[tid] : -1;
   if (tid == 0) *pool_size_g = n_pool;
 
   // ---- per-source tables (Eq. minimum_loss_assignment over the pool) ----
   pool_tables(N, S, L, pool, in_pool, n_pool, tgt, scl, tgt_g, scl_g);
   }  // dynamic
-  __syncthreads();
+  lds_barrier();
 
   // ---- remap every slot (Eq. decode_remap); retained slots copied ----
   for (int j = tid; j < slots; j += kPoolThreads) {
@@ -717,7 +719,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     sw[j] = wn;
     atomicAdd(&rows_of[te], 1);
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- group offsets and GEMM m-tile lists: wave 0, five groups per lane ----
   if (wave == 0) {
@@ -748,7 +750,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     er -= sr;
     ea -= sa;
     eb -= sb;
-    const int ta = __shfl(ea + sa, kWave - 1, kWave), tb = __shfl(eb + sb, kWave - 1, kWave);
+    const int ta = (int)readlane_u32((uint32_t)(ea + sa), kWave - 1), tb = (int)readlane_u32((uint32_t)(eb + sb), kWave - 1);
 #pragma unroll
     for (int q = 0; q < G; ++q) {
       const int g = lane * G + q;
@@ -767,7 +769,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
 #pragma unroll
     for (int q = 0; q < kFrontWaves; ++q) wcnt[q][e] = 0;
   }
-  __syncthreads();
+  lds_barrier();
 
   // ---- stable scatter: rounds of kPoolThreads slots in slot order ----
   for (int base = 0; base < slots; base += kPoolThreads) {
@@ -784,7 +786,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     }
     const int rank = __popcll(m & lanemask_lt(lane));
     if (valid && rank == 0) wcnt[wave][e] = __popcll(m);
-    __syncthreads();
+    lds_barrier();
     if (valid) {
       int pos = cur[e] + rank;
       for (int q = 0; q < wave; ++q) pos += wcnt[q][e];
@@ -793,7 +795,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
       row_w[pos] = sw[j];
       slot_row[j] = pos;
     }
-    __syncthreads();
+    lds_barrier();
     for (int x = tid; x < N; x += kPoolThreads) {
       int add = 0;
 #pragma unroll
@@ -803,7 +805,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
       }
       cur[x] += add;
     }
-    __syncthreads();
+    lds_barrier();
   }
   // Shared-expert rows follow the routed rows, one per token, weight 1.
   for (int i = tid; i < t_shared; i += kPoolThreads) {
