@@ -170,13 +170,23 @@ hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, 
 __device__ __forceinline__ void wave_logit_row(const float *__restrict__ part, int P, int T, int N,
                                                const float *__restrict__ bias, int t, int lane,
                                                float *__restrict__ out, float v[4]) {
+  // the slices are loaded eight at a time (one latency per eight) and added in order
+  constexpr int kBatch = 8;
 #pragma unroll
   for (int j = 0; j < 4; ++j) {
     const int e = lane + 64 * j;
     float a = 0.f;
     if (e < N) {
-      a = part[(size_t)t * N + e];
-      for (int z = 1; z < P; ++z) a += part[((size_t)z * T + t) * N + e];
+      const float *col = part + (size_t)t * N + e;
+      const size_t zs = (size_t)T * N;
+      for (int z0 = 0; z0 < P; z0 += kBatch) {
+        float pv[kBatch];
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b) pv[b] = (z0 + b < P) ? col[(size_t)(z0 + b) * zs] : 0.f;
+#pragma unroll
+        for (int b = 0; b < kBatch; ++b)
+          if (z0 + b < P) a = (z0 + b == 0) ? pv[b] : a + pv[b];
+      }
       if (bias) a += bias[e];
       if (out) out[(size_t)t * N + e] = a;
     }
