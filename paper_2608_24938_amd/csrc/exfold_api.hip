@@ -164,12 +164,15 @@ exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
   a.Y = p.direct ? nullptr : at<float>(ws, p.o_Y);
   a.y = y;
   a.direct = p.direct;
+  // rows that only the combine reads travel as bf16 (each term rounded once
+  // before the fp32 sum over the token's routes); kept rows stay fp32
+  a.y_bf16 = p.dtype == EXFOLD_BF16 && !p.direct && !keep_rows && p.dn.ksplit == 1;
   hipEvent_t ev_mid = (events && events[EXFOLD_EV_GATE_UP])
                           ? static_cast<hipEvent_t>(events[EXFOLD_EV_GATE_UP]) : nullptr;
   if (launch_expert_gemms(a, p.gu, p.dn, s, ev_mid) != hipSuccess) return EXFOLD_ERR_DEVICE;
   record(events, EXFOLD_EV_DOWN, s);
   if (!p.direct && !keep_rows) {
-    if (launch_combine(p.dtype, a.Y, p.dn.ksplit, p.rows, pb.slot_row, p.T, p.k_out, p.d,
+    if (launch_combine(p.dtype, a.Y, a.y_bf16, p.dn.ksplit, p.rows, pb.slot_row, p.T, p.k_out, p.d,
                        p.t_shared > 0 ? p.R : -1, y, s) != hipSuccess)
       return EXFOLD_ERR_DEVICE;
   }

@@ -35,6 +35,7 @@ struct GemmKArgs {
   int d;                 // down: output width
   bf16_t *H;
   float *Y;
+  bf16_t *Yh;  // down, when set: bf16 per-row outputs instead of Y (no split)
   bf16_t *y;
   const float *row_w;
 };
@@ -284,7 +285,10 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
             if (DIRECT)
               p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v);
             else
-              p.Y[((long long)t.ks * p.rows + row) * p.d + n] = v;
+              if (p.Yh)
+                p.Yh[(long long)row * p.d + n] = f32_to_bf16(v);
+              else
+                p.Y[((long long)t.ks * p.rows + row) * p.d + n] = v;
           }
         }
       }
@@ -442,6 +446,8 @@ __global__ __launch_bounds__(256) void expert_gemm_skinny(const GemmKArgs p) {
           const int n = t.nt * kSkN + j * 32 + (lane & 31);
           if (DIRECT)
             p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(acc[j][q] * w);
+          else if (p.Yh)
+            p.Yh[(long long)row * p.d + n] = f32_to_bf16(acc[j][q] * w);
           else
             p.Y[((long long)t.ks * p.rows + row) * p.d + n] = acc[j][q] * w;
         }
@@ -617,7 +623,8 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
   da.ldw = a.inter;
   da.inter = a.inter;
   da.d = a.d;
-  da.Y = a.Y;
+  da.Y = a.y_bf16 ? nullptr : a.Y;
+  da.Yh = a.y_bf16 ? reinterpret_cast<bf16_t *>(a.Y) : nullptr;
   da.y = static_cast<bf16_t *>(a.y);
   da.row_w = a.row_w;
 
@@ -648,8 +655,21 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
 // Weighted combine: y_i = sum_k Y[row(i,k)] (+ shared row), in slot order;
 // float32 accumulation, one rounding to the output dtype.
 // ---------------------------------------------------------------------------
-template <typename OutT>
-__global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ Y, int ksplit,
+template <typename InT>
+__device__ __forceinline__ float4 load4(const InT *p);
+template <>
+__device__ __forceinline__ float4 load4<float>(const float *p) {
+  return *reinterpret_cast<const float4 *>(p);
+}
+template <>
+__device__ __forceinline__ float4 load4<bf16_t>(const bf16_t *p) {
+  const uint2 u = *reinterpret_cast<const uint2 *>(p);
+  return make_float4(__uint_as_float(u.x << 16), __uint_as_float(u.x & 0xffff0000u),
+                     __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
+}
+
+template <typename InT, typename OutT>
+__global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y, int ksplit,
                                                      int rows, const int32_t *__restrict__ slot_row,
                                                      int k_out, int d, int shared_base,
                                                      OutT *__restrict__ y) {
@@ -667,7 +687,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
       else
         break;
       for (int sp = 0; sp < ksplit; ++sp) {
-        const float4 v = *reinterpret_cast<const float4 *>(Y + sp * split + r * d + c);
+        const float4 v = load4<InT>(Y + sp * split + r * d + c);
         acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
       }
     }
@@ -679,16 +699,21 @@ __global__ __launch_bounds__(256) void combine_kernel(const float *__restrict__ 
   }
 }
 
-hipError_t launch_combine(int dtype, const float *Y, int ksplit, int rows, const int32_t *slot_row,
-                          int T, int k_out, int d, int shared_base, void *y, hipStream_t s) {
+hipError_t launch_combine(int dtype, const float *Y, bool y_bf16, int ksplit, int rows,
+                          const int32_t *slot_row, int T, int k_out, int d, int shared_base, void *y,
+                          hipStream_t s) {
   if (T <= 0) return hipSuccess;
   const dim3 grid(T, (d + 1023) / 1024);
-  if (dtype == EXFOLD_BF16)
-    combine_kernel<bf16_t><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
-                                                static_cast<bf16_t *>(y));
+  if (dtype == EXFOLD_BF16 && y_bf16)
+    combine_kernel<bf16_t, bf16_t><<<grid, 256, 0, s>>>(reinterpret_cast<const bf16_t *>(Y), ksplit,
+                                                        rows, slot_row, k_out, d, shared_base,
+                                                        static_cast<bf16_t *>(y));
+  else if (dtype == EXFOLD_BF16)
+    combine_kernel<float, bf16_t><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
+                                                       static_cast<bf16_t *>(y));
   else
-    combine_kernel<float><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
-                                               static_cast<float *>(y));
+    combine_kernel<float, float><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
+                                                      static_cast<float *>(y));
   return hipGetLastError();
 }
 

@@ -88,6 +88,7 @@ struct ExpertArgs {
   float *Y;     // [ksplit, rows, d] per-row outputs (nullptr when direct)
   void *y;      // [T, d] direct output (each token owns exactly one row)
   bool direct;
+  bool y_bf16;  // bf16 GEMMs, no split: Y holds [rows, d] bf16 rows instead
 };
 // active_groups: expected number of non-empty groups (sizes the down split).
 void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d, int inter,
@@ -95,8 +96,9 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
 // ev_mid (optional) is recorded between the gate_up and the down GEMM.
 hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const GemmPlan &dn,
                                hipStream_t s, hipEvent_t ev_mid = nullptr);
-hipError_t launch_combine(int dtype, const float *Y, int ksplit, int rows, const int32_t *slot_row,
-                          int T, int k_out, int d, int shared_base, void *y, hipStream_t s);
+hipError_t launch_combine(int dtype, const float *Y, bool y_bf16, int ksplit, int rows,
+                          const int32_t *slot_row, int T, int k_out, int d, int shared_base, void *y,
+                          hipStream_t s);
 
 // ---- diagonal projectors (k_diag.hip) ----
 // Per-pair per-dimension statistics -> Dg [N, N, d] and the diagonal loss Ld [N, N].
