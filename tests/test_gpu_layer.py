@@ -225,6 +225,8 @@ def test_zero_tokens_is_a_noop():
 PATH_SHAPES = {
     "bf16-256x512": synth.LayerShape("paths", d=256, inter=512, n_experts=8, top_k=2, dtype="bf16"),
     "bf16-384x192": synth.LayerShape("paths-odd", d=384, inter=192, n_experts=8, top_k=2, dtype="bf16"),
+    # six 64-wide reduction stages and two 128-column gate/up slices on the wide gate/up tile
+    "bf16-384x256": synth.LayerShape("paths-384", d=384, inter=256, n_experts=8, top_k=2, dtype="bf16"),
 }
 
 
