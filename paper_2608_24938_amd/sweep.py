@@ -22,7 +22,7 @@ Mixtral-, Qwen3- and GLM-shaped prefill and decode cases) on one GPU:
   of the HBM peak.
 
     python -m paper_2608_24938_amd.sweep [--only NAME ...] [--reps-prefill 20] [--reps-decode 100]
-                                         [--md FILE]
+                                         [--md FILE] [--ceilings]
 
 Prints one JSON line per configuration; --md also writes a markdown table.
 """
@@ -161,6 +161,35 @@ def run_config(name, wl, layer, dev, args, ev, stream, scratch):
     return rec
 
 
+def ceilings(ev, stream):
+    """Context for the fractions: a large plain bf16 GEMM through torch (hipBLASLt), a streaming read
+    of 4 GiB through torch's reduction and a 2 GiB device copy (read + write bytes), each the median of
+    10 timed calls."""
+    import torch
+    out = {}
+    n = 8192
+    a = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    b = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    for _ in range(3):
+        torch.matmul(a, b)
+    us = _time(None, ev, stream, lambda: torch.matmul(a, b), 10, None)
+    out["bf16_gemm_8192_tflops"] = round(2 * n ** 3 / (float(np.median(us)) * 1e-6) / 1e12, 1)
+    del a, b
+    big = torch.ones(1 << 30, dtype=torch.float32, device="cuda")  # 4 GiB
+    for _ in range(2):
+        big.sum()
+    us = _time(None, ev, stream, lambda: big.sum(), 10, None)
+    out["stream_read_4gib_gbs"] = round(big.numel() * 4 / (float(np.median(us)) * 1e-6) / 1e9, 1)
+    half = big[: big.numel() // 2]
+    dst = torch.empty_like(half)
+    dst.copy_(half)
+    us = _time(None, ev, stream, lambda: dst.copy_(half), 10, None)
+    out["stream_copy_2gib_read_plus_write_gbs"] = round(2 * half.numel() * 4 / (float(np.median(us)) * 1e-6) / 1e9, 1)
+    del big, half, dst
+    torch.cuda.empty_cache()
+    return out
+
+
 def markdown(recs):
     lines = ["| config | µs cold (p10–p90) | µs warm | µs graph | µs unfolded | 8 batches | touched | "
              "rows max/mean | fold overhead | rate | % peak |", "|---|---|---|---|---|---|---|---|---|---|---|"]
@@ -187,6 +216,8 @@ def main(argv=None):
     ap.add_argument("--reps-decode", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--md", help="also write a markdown table here")
+    ap.add_argument("--ceilings", action="store_true",
+                    help="also time a plain 8192^3 bf16 GEMM, a 4 GiB streaming read and a 2 GiB copy (context)")
     args = ap.parse_args(argv)
 
     import torch
@@ -201,6 +232,8 @@ def main(argv=None):
     ev = HipEvents()
     scratch = torch.empty(SCRATCH_BYTES // 4, dtype=torch.float32, device="cuda")
     recs = []
+    if args.ceilings:
+        print(json.dumps({"ceilings": ceilings(ev, stream)}), flush=True)
     # one layer per shape, configurations of a shape in a row
     by_shape = {}
     for n in names:
