@@ -49,7 +49,7 @@ from paper_2608_24938_amd.measure import (PEAK_BF16_TFLOPS, PEAK_HBM_GBS, HipEve
 
 METRIC = "folded MoE layer: prefill TFLOP/s + %MFMA peak; decode µs/layer + HBM GB/s"
 COPY_BYTES = 1 << 30        # size of the calibration copy
-DOMINANT = "expert_gemm_tile<128, 128, 2, true, false>"   # gate/up GEMM with fused SiLU*up
+DOMINANT = "expert_gemm_wide<64, 2>"   # prefill gate/up GEMM with fused SiLU*up (256x256 tiles)
 KERNEL_SOURCES = ["paper_2608_24938_amd/csrc/k_gemm.hip", "paper_2608_24938_amd/csrc/common.hpp",
                   "paper_2608_24938_amd/csrc/kernels.hpp", "paper_2608_24938_amd/build.py"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "expert_gemm_gate_up_mixtral_prefill_traffic.md")

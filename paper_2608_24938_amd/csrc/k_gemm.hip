@@ -297,6 +297,179 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
 }
 
 // ---------------------------------------------------------------------------
+// Wide tile for the prefill gate/up GEMM (many rows per retained expert):
+// 256x256 macro tile, eight waves (two per SIMD), wave (wm, wn) owning tile
+// rows 128 wm .. 128 wm + 127 and gate columns 32 wn .. 32 wn + 31 with the
+// matching up columns (4x2 MFMA tiles).  The operands go from global memory
+// straight into LDS (global_load_lds_dwordx4) through a ring of reduction
+// stages: no staging registers and no LDS write instructions.  Against 128x128
+// tiles the bytes loaded per flop halve, and the weight panel a tile shares
+// with the other m-tiles of its expert is fetched from HBM about once (2.4 GB
+// per Mixtral-shaped launch against 3.8-5 GB).  Measured on that launch, the
+// 64-wide stages with two ring buffers beat 32-wide stages with four or five
+// buffers (more bytes in flight, but 64-byte row pieces and twice the barriers).
+// ---------------------------------------------------------------------------
+constexpr int kWide = 256, kWideThreads = 512, kWideBK = 64, kWideStages = 2;
+
+// LDS byte address of a shared-memory pointer (for M0).
+__device__ __forceinline__ uint32_t lds_addr(const void *ptr) {
+  return (uint32_t)(uintptr_t)(const __attribute__((address_space(3))) void *)ptr;
+}
+
+// One 16-byte chunk per lane from global g into the 1 KiB LDS block at byte
+// address lds (wave-uniform): lane l lands at lds + 16 l.  M0 holds the block
+// address; one wait state separates its write from the load.
+__device__ __forceinline__ void lds_dma16(const void *g, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
+               :
+               : "v"(g), "s"(lds)
+               : "memory", "m0");
+}
+
+// Slot of 16-byte chunk q in a tile row of BK bf16 (an involution in q): the
+// chunk columns that one ds_read_b128 takes from consecutive rows land in
+// distinct LDS banks.  64-byte rows: q ^ bits 2..3 of r; 128-byte rows: the
+// Gray-code swizzle of the register-staged tiles.
+template <int BK>
+__device__ __forceinline__ int wide_slot(int r, int q) {
+  if (BK == 32) return q ^ ((r >> 2) & 3);
+  return q ^ ((r ^ (r >> 1)) & 7);
+}
+
+template <int BK, int STAGES>
+__global__ __launch_bounds__(kWideThreads, 1) void expert_gemm_wide(const GemmKArgs p) {
+  constexpr int BM = kWide, BN = kWide, TM = 4, TN = 2;
+  constexpr int STAGE = (BM + BN) * BK;          // elements of one stage (A rows, then B rows)
+  constexpr int CPR = BK / 8;                    // 16-byte chunks per row
+  constexpr int RPB = 64 / CPR;                  // rows per 1 KiB block
+  constexpr int BLOCKS = (BM + BN) / RPB;        // blocks per stage
+  constexpr int PW = BLOCKS / (kWideThreads / 64);  // DMA loads per wave per stage
+  constexpr int AHEAD = STAGES - 1;              // stages in flight while one is computed
+  constexpr int VMC = (AHEAD - 1) * PW;          // loads allowed in flight at a stage's wait
+  static_assert(VMC == 0 || VMC == 8 || VMC == 12 || VMC == 16, "vmcnt immediates below");
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[STAGES * STAGE];
+
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int wm = wave >> 2, wn = wave & 3;
+
+  TileId t;
+  if (!decode_tile(p, blockIdx.x, t)) return;
+  const int row0 = p.offsets[t.g] + t.mt * BM;
+  const int valid = min(BM, p.offsets[t.g + 1] - row0);
+  const bf16_t *Wg = (t.g < p.n_experts) ? p.W + (long long)t.g * p.w_stride : p.Ws;
+
+  // Wave w fills blocks w, w + 8, ...; lane l fills row RPB b + l / CPR of its
+  // block at slot l % CPR, i.e. it fetches the chunk that the swizzle puts
+  // there.  Rows past the group's end re-read its first row (in bounds, never
+  // stored).
+  const bf16_t *src[PW];
+#pragma unroll
+  for (int i = 0; i < PW; ++i) {
+    const int blk = i * 8 + wave;
+    const int r = blk * RPB + lane / CPR;  // stage row: A rows 0..255, then B rows
+    if (r < BM) {
+      const int q = wide_slot<BK>(r, lane % CPR);
+      const int rr = row0 + (r < valid ? r : 0);
+      src[i] = p.A + (long long)p.row_token[rr] * p.lda + q * 8;
+    } else {
+      const int rb = r - BM;
+      const int q = wide_slot<BK>(rb, lane % CPR);
+      const int wrow = (rb < BN / 2) ? t.nt * (BN / 2) + rb : p.inter + t.nt * (BN / 2) + (rb - BN / 2);
+      src[i] = Wg + (long long)wrow * p.ldw + q * 8;
+    }
+  }
+  const uint32_t lds0 = lds_addr(smem);
+
+  f32x16 acc[TM][TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i)
+#pragma unroll
+    for (int j = 0; j < TN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
+  int a_row[TM], b_row[TN];
+#pragma unroll
+  for (int i = 0; i < TM; ++i) a_row[i] = wm * 128 + i * 32 + (lane & 31);
+#pragma unroll
+  for (int j = 0; j < TN; ++j) b_row[j] = j * (BN / 2) + wn * 32 + (lane & 31);
+
+  const int KT = p.kc / BK;
+  // Stage kt (clamped to the last: loads past the end refill a buffer that is
+  // never read again) into ring buffer BUF.
+#define EXF_W_ISSUE(BUF, KT_)                                                                  \
+  do {                                                                                         \
+    const int k0_ = min((KT_), KT - 1) * BK;                                                   \
+    const uint32_t base_ = lds0 + (uint32_t)(BUF) * (STAGE * 2);                               \
+    _Pragma("unroll") for (int i_ = 0; i_ < PW; ++i_)                                          \
+        lds_dma16(src[i_] + k0_, base_ + (i_ * 8 + wave) * 1024);                              \
+  } while (0)
+#define EXF_W_FRAGS(A_, B_, BUF, S_)                                                           \
+  do {                                                                                         \
+    const bf16_t *As_ = smem + (BUF) * STAGE;                                                  \
+    const bf16_t *Bs_ = As_ + BM * BK;                                                         \
+    const int ch_ = (S_) * 2 + (lane >> 5);                                                    \
+    _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_) A_[i_] = *reinterpret_cast<const bf16x8 *>( \
+        As_ + a_row[i_] * BK + wide_slot<BK>(a_row[i_], ch_) * 8);                             \
+    _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) B_[j_] = *reinterpret_cast<const bf16x8 *>( \
+        Bs_ + b_row[j_] * BK + wide_slot<BK>(b_row[j_], ch_) * 8);                             \
+  } while (0)
+#define EXF_W_MMA(A_, B_)                                                                      \
+  do {                                                                                         \
+    _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_)                                          \
+        _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) acc[i_][j_] =                        \
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(A_[i_], B_[j_], acc[i_][j_], 0, 0, 0);     \
+  } while (0)
+
+  for (int q = 0; q < AHEAD; ++q) EXF_W_ISSUE(q, q);
+  int buf = 0;  // ring buffer of stage kt (wave-uniform)
+  for (int kt = 0; kt < KT; ++kt) {
+    // Wait until this wave's loads of stage kt have landed (the later stages
+    // stay in flight) and its LDS reads of the previous stage are done; after
+    // the barrier every wave's part of stage kt is in LDS and nobody reads the
+    // previous buffer any more, so it is refilled with stage kt + AHEAD; then
+    // the k16 steps of stage kt.
+    if (VMC == 0)
+      asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else if (VMC == 8)
+      asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else if (VMC == 12)
+      asm volatile("s_waitcnt vmcnt(12) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    const int prev = (buf == 0) ? STAGES - 1 : buf - 1;
+    EXF_W_ISSUE(prev, kt + AHEAD);
+#pragma unroll
+    for (int s2 = 0; s2 < BK / 32; ++s2) {
+      bf16x8 a0_[TM], b0_[TN], a1_[TM], b1_[TN];
+      EXF_W_FRAGS(a0_, b0_, buf, 2 * s2);
+      EXF_W_FRAGS(a1_, b1_, buf, 2 * s2 + 1);
+      EXF_W_MMA(a0_, b0_);
+      EXF_W_MMA(a1_, b1_);
+    }
+    buf = (buf == STAGES - 1) ? 0 : buf + 1;
+  }
+  // the clamped loads past the end must land before the workgroup's LDS is released
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+#undef EXF_W_ISSUE
+#undef EXF_W_FRAGS
+#undef EXF_W_MMA
+
+  // ---- epilogue: H = SiLU(gate) * up ----
+#pragma unroll
+  for (int i = 0; i < TM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int ml = wm * 128 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+      if (ml < valid) {
+        const int n = t.nt * (BN / 2) + wn * 32 + (lane & 31);
+        p.H[(long long)(row0 + ml) * p.inter + n] = f32_to_bf16(silu(acc[i][0][r]) * acc[i][1][r]);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
 // Skinny tile for decode (few rows per retained expert): 32 rows x 64 output
 // columns (gate/up: 32 gate + 32 up columns), BK = 128 per stage (256 contiguous
 // bytes of every weight row per load step), and the four waves split each
@@ -545,10 +718,18 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
   const bool sk_shapes = inter % 128 == 0 && d % 64 == 0;
   const int mt128 = (rows + 127) / 128 > active ? (rows + 127) / 128 : active;
   const bool gu_skinny = sk_shapes && (rows <= 24 * active || mt128 * (inter / 64) < cu_count);
+  // Many rows per retained expert (prefill, at least one and a half 256-row
+  // tiles on average): 256x256 gate/up tiles.  Below that the partial tiles of
+  // a skewed load cost more than the wide tile saves (Qwen3-shaped prefill,
+  // 256 rows per expert: even).
+  const bool gu_wide = !gu_skinny && inter % 128 == 0 && d % 128 == 0 && 2 * rows >= 3 * kWide * active;
   const bool dn_skinny = sk_shapes && rows <= 64 * active;
   if (gu_skinny) {
     *gu = GemmPlan{kSkM, kSkN, 1, 0, kGemmSkinny};
     gu->grid = (rows / kSkM + groups) * (inter / (kSkN / 2));  // >= sum of ceil(rows_g / 32) tiles
+  } else if (gu_wide) {
+    *gu = GemmPlan{kWide, kWide, 1, 0, kGemmWide};
+    gu->grid = (rows / kWide + groups) * (inter / (kWide / 2));
   } else {
     *gu = GemmPlan{128, 128, 1, 0, kGemmTile};
     gu->grid = (rows / 128 + groups) * (inter / 64);
@@ -631,6 +812,8 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
   if (gu.grid > 0) {
     if (gu.kind == kGemmSkinny)
       expert_gemm_skinny<true, false><<<gu.grid, 256, 0, s>>>(ga);
+    else if (gu.kind == kGemmWide)
+      expert_gemm_wide<kWideBK, kWideStages><<<gu.grid, kWideThreads, 0, s>>>(ga);
     else
       expert_gemm_tile<128, 128, 2, true, false><<<gu.grid, 256, 0, s>>>(ga);
   }

@@ -66,13 +66,14 @@ hipError_t launch_static_pool(const float *h, int N, int D, const float *S, cons
                               hipStream_t s);
 
 // ---- expert GEMMs and combine (k_gemm.hip) ----
-// kGemmTile: 128x128 tiles; kGemmSkinny: 32x64 tiles for few rows per expert.
-enum { kGemmSimt = 0, kGemmTile = 1, kGemmSkinny = 2 };
+// kGemmTile: 128x128 tiles; kGemmSkinny: 32x64 tiles for few rows per expert;
+// kGemmWide: 256x256 gate/up tiles (eight waves, loads straight into LDS).
+enum { kGemmSimt = 0, kGemmTile = 1, kGemmSkinny = 2, kGemmWide = 3 };
 struct GemmPlan {
   int bm, bn;  // tile height (rows) and width (output columns, or weight rows for gate/up)
   int ksplit;  // splits of the reduction (down projection only; partial outputs)
   int grid;    // workgroups launched (an upper bound on the device-side tile count)
-  int kind;    // kGemmSimt (float32 layers), kGemmTile or kGemmSkinny (bf16 MFMA tiles)
+  int kind;    // kGemmSimt (float32 layers), kGemmTile, kGemmSkinny or kGemmWide (bf16 MFMA tiles)
 };
 struct ExpertArgs {
   int dtype;
