@@ -23,11 +23,13 @@ WIDE_BF16 = synth.LayerShape("wide-bf16", d=256, inter=128, n_experts=128, top_k
                              router_bias=True, m_cal=1024)
 SHARED_BF16 = synth.LayerShape("shared-bf16", d=384, inter=192, n_experts=64, top_k=6, shared_inter=192,
                                dtype="bf16", m_cal=512)
+# 4096 tokens on 8 experts: the gate/up GEMM takes the wide tile loaded straight into LDS
+DEEP_BF16 = synth.LayerShape("deep-bf16", d=256, inter=512, n_experts=8, top_k=2, dtype="bf16")
 
 
 @pytest.mark.parametrize("shape,T,phase,budget", [(WIDE_BF16, 300, "prefill", 4), (WIDE_BF16, 48, "decode", 16),
                                                   (SHARED_BF16, 40, "decode", 8), (synth.TINY, 64, "prefill", 1),
-                                                  (WIDE_BF16, 48, "dense", 8)])
+                                                  (WIDE_BF16, 48, "dense", 8), (DEEP_BF16, 4096, "prefill", 1)])
 def test_graph_replays_match_eager(shape, T, phase, budget):
     lp = LayerPair(shape, seed=21)
     S, L, h = (to_dev(a) for a in synth.synthetic_tables(shape.n_experts, seed=21))
