@@ -309,7 +309,7 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
 // 64-wide stages with two ring buffers beat 32-wide stages with four or five
 // buffers (more bytes in flight, but 64-byte row pieces and twice the barriers).
 // ---------------------------------------------------------------------------
-constexpr int kWide = 256, kWideThreads = 512, kWideBK = 64, kWideStages = 2;
+constexpr int kWide = 256, kWideWaves = 8, kWideBK = 64, kWideStages = 2;
 
 // LDS byte address of a shared-memory pointer (for M0).
 __device__ __forceinline__ uint32_t lds_addr(const void *ptr) {
@@ -336,22 +336,25 @@ __device__ __forceinline__ int wide_slot(int r, int q) {
   return q ^ ((r ^ (r >> 1)) & 7);
 }
 
-template <int BK, int STAGES>
-__global__ __launch_bounds__(kWideThreads, 1) void expert_gemm_wide(const GemmKArgs p) {
-  constexpr int BM = kWide, BN = kWide, TM = 4, TN = 2;
+template <int BK, int STAGES, int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void expert_gemm_wide(const GemmKArgs p) {
+  // NW waves in two rows of NW / 2; each wave owns 128 rows and 32 gate + 32 up columns
+  constexpr int NT = 64 * NW, WN = NW / 2;
+  constexpr int BM = kWide, BN = 64 * WN, TM = 4, TN = 2;
   constexpr int STAGE = (BM + BN) * BK;          // elements of one stage (A rows, then B rows)
   constexpr int CPR = BK / 8;                    // 16-byte chunks per row
   constexpr int RPB = 64 / CPR;                  // rows per 1 KiB block
   constexpr int BLOCKS = (BM + BN) / RPB;        // blocks per stage
-  constexpr int PW = BLOCKS / (kWideThreads / 64);  // DMA loads per wave per stage
+  constexpr int PW = BLOCKS / NW;                 // DMA loads per wave per stage
   constexpr int AHEAD = STAGES - 1;              // stages in flight while one is computed
   constexpr int VMC = (AHEAD - 1) * PW;          // loads allowed in flight at a stage's wait
-  static_assert(VMC == 0 || VMC == 8 || VMC == 12 || VMC == 16, "vmcnt immediates below");
+  static_assert(VMC == 0 || VMC == 6 || VMC == 8 || VMC == 12 || VMC == 16, "vmcnt immediates below");
+  static_assert(BLOCKS % NW == 0, "blocks per wave");
   __shared__ __attribute__((aligned(1024))) bf16_t smem[STAGES * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WN, wn = wave % WN;
 
   TileId t;
   if (!decode_tile(p, blockIdx.x, t)) return;
@@ -359,14 +362,14 @@ __global__ __launch_bounds__(kWideThreads, 1) void expert_gemm_wide(const GemmKA
   const int valid = min(BM, p.offsets[t.g + 1] - row0);
   const bf16_t *Wg = (t.g < p.n_experts) ? p.W + (long long)t.g * p.w_stride : p.Ws;
 
-  // Wave w fills blocks w, w + 8, ...; lane l fills row RPB b + l / CPR of its
+  // Wave w fills blocks w, w + NW, ...; lane l fills row RPB b + l / CPR of its
   // block at slot l % CPR, i.e. it fetches the chunk that the swizzle puts
   // there.  Rows past the group's end re-read its first row (in bounds, never
   // stored).
   const bf16_t *src[PW];
 #pragma unroll
   for (int i = 0; i < PW; ++i) {
-    const int blk = i * 8 + wave;
+    const int blk = i * NW + wave;
     const int r = blk * RPB + lane / CPR;  // stage row: A rows 0..255, then B rows
     if (r < BM) {
       const int q = wide_slot<BK>(r, lane % CPR);
@@ -402,7 +405,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void expert_gemm_wide(const GemmKA
     const int k0_ = min((KT_), KT - 1) * BK;                                                   \
     const uint32_t base_ = lds0 + (uint32_t)(BUF) * (STAGE * 2);                               \
     _Pragma("unroll") for (int i_ = 0; i_ < PW; ++i_)                                          \
-        lds_dma16(src[i_] + k0_, base_ + (i_ * 8 + wave) * 1024);                              \
+        lds_dma16(src[i_] + k0_, base_ + (i_ * NW + wave) * 1024);                             \
   } while (0)
 #define EXF_W_FRAGS(A_, B_, BUF, S_)                                                           \
   do {                                                                                         \
@@ -431,6 +434,8 @@ __global__ __launch_bounds__(kWideThreads, 1) void expert_gemm_wide(const GemmKA
     // the k16 steps of stage kt.
     if (VMC == 0)
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+    else if (VMC == 6)
+      asm volatile("s_waitcnt vmcnt(6) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     else if (VMC == 8)
       asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     else if (VMC == 12)
@@ -728,8 +733,8 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
     *gu = GemmPlan{kSkM, kSkN, 1, 0, kGemmSkinny};
     gu->grid = (rows / kSkM + groups) * (inter / (kSkN / 2));  // >= sum of ceil(rows_g / 32) tiles
   } else if (gu_wide) {
-    *gu = GemmPlan{kWide, kWide, 1, 0, kGemmWide};
-    gu->grid = (rows / kWide + groups) * (inter / (kWide / 2));
+    *gu = GemmPlan{kWide, 64 * (kWideWaves / 2), 1, 0, kGemmWide};
+    gu->grid = (rows / kWide + groups) * (inter / (32 * (kWideWaves / 2)));
   } else {
     *gu = GemmPlan{128, 128, 1, 0, kGemmTile};
     gu->grid = (rows / 128 + groups) * (inter / 64);
@@ -813,7 +818,7 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
     if (gu.kind == kGemmSkinny)
       expert_gemm_skinny<true, false><<<gu.grid, 256, 0, s>>>(ga);
     else if (gu.kind == kGemmWide)
-      expert_gemm_wide<kWideBK, kWideStages><<<gu.grid, kWideThreads, 0, s>>>(ga);
+      expert_gemm_wide<kWideBK, kWideStages, kWideWaves><<<gu.grid, 64 * kWideWaves, 0, s>>>(ga);
     else
       expert_gemm_tile<128, 128, 2, true, false><<<gu.grid, 256, 0, s>>>(ga);
   }
