@@ -36,6 +36,7 @@ struct GemmKArgs {
   bf16_t *H;
   float *Y;
   bf16_t *Yh;  // down, when set: bf16 per-row outputs instead of Y (no split)
+  float *P;    // down, stream-K: partial tiles [2 * workgroups][256 * 256]
   bf16_t *y;
   const float *row_w;
 };
@@ -57,11 +58,9 @@ __device__ __forceinline__ int swz(int r, int q) { return (r * 8 + (q ^ ((r ^ (r
 struct TileId {
   int g, nt, ks, mt;
 };
-__device__ __forceinline__ bool decode_tile(const GemmKArgs &p, int wg, TileId &t) {
+// Tile of logical id L (m-tile fastest within a group and n-tile).
+__device__ __forceinline__ void tile_at(const GemmKArgs &p, int L, TileId &t) {
   const int units = p.n_tiles * p.ksplit;
-  const int total = p.tile_start[p.groups] * units;
-  if (wg >= total) return false;
-  const int L = xcd_remap(wg, total);
   int lo = 0, hi = p.groups;
   while (hi - lo > 1) {
     const int mid = (lo + hi) >> 1;
@@ -74,6 +73,13 @@ __device__ __forceinline__ bool decode_tile(const GemmKArgs &p, int wg, TileId &
   const int u = local / mt_g;
   t.ks = u % p.ksplit;
   t.nt = u / p.ksplit;
+}
+
+__device__ __forceinline__ bool decode_tile(const GemmKArgs &p, int wg, TileId &t) {
+  const int units = p.n_tiles * p.ksplit;
+  const int total = p.tile_start[p.groups] * units;
+  if (wg >= total) return false;
+  tile_at(p, xcd_remap(wg, total), t);
   return true;
 }
 
@@ -310,6 +316,7 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
 // buffers (more bytes in flight, but 64-byte row pieces and twice the barriers).
 // ---------------------------------------------------------------------------
 constexpr int kWide = 256, kWideWaves = 8, kWideBK = 64, kWideStages = 2;
+constexpr bool kWideDown = false;
 
 // LDS byte address of a shared-memory pointer (for M0).
 __device__ __forceinline__ uint32_t lds_addr(const void *ptr) {
@@ -336,30 +343,33 @@ __device__ __forceinline__ int wide_slot(int r, int q) {
   return q ^ ((r ^ (r >> 1)) & 7);
 }
 
-template <int BK, int STAGES, int NW>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void expert_gemm_wide(const GemmKArgs p) {
-  // NW waves in two rows of NW / 2; each wave owns 128 rows and 32 gate + 32 up columns
-  constexpr int NT = 64 * NW, WN = NW / 2;
-  constexpr int BM = kWide, BN = 64 * WN, TM = 4, TN = 2;
+constexpr int kWideTM = 4, kWideTN = 2;  // 32x32 MFMA tiles per wave
+
+// Main loop of one wide tile over the reduction stages [k0, k1): zeroes acc,
+// streams the stages through the LDS ring and leaves the products in acc.
+// All waves of the workgroup call it; it ends with every load landed and a
+// barrier, so the ring may be refilled right after.
+template <bool GATE_UP, int BK, int STAGES, int NW>
+__device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &t, int row0, int valid,
+                                              int k0, int k1, bf16_t *smem,
+                                              f32x16 (&acc)[kWideTM][kWideTN]) {
+  // NW waves in two rows of NW / 2; each wave owns 128 rows and 64 output columns
+  // (gate/up: 32 gate + 32 up columns)
+  constexpr int WN = NW / 2;
+  constexpr int BM = kWide, BN = 64 * WN, TM = kWideTM, TN = kWideTN;
   constexpr int STAGE = (BM + BN) * BK;          // elements of one stage (A rows, then B rows)
   constexpr int CPR = BK / 8;                    // 16-byte chunks per row
   constexpr int RPB = 64 / CPR;                  // rows per 1 KiB block
   constexpr int BLOCKS = (BM + BN) / RPB;        // blocks per stage
-  constexpr int PW = BLOCKS / NW;                 // DMA loads per wave per stage
+  constexpr int PW = BLOCKS / NW;                // DMA loads per wave per stage
   constexpr int AHEAD = STAGES - 1;              // stages in flight while one is computed
   constexpr int VMC = (AHEAD - 1) * PW;          // loads allowed in flight at a stage's wait
   static_assert(VMC == 0 || VMC == 6 || VMC == 8 || VMC == 12 || VMC == 16, "vmcnt immediates below");
   static_assert(BLOCKS % NW == 0, "blocks per wave");
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[STAGES * STAGE];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / WN, wn = wave % WN;
-
-  TileId t;
-  if (!decode_tile(p, blockIdx.x, t)) return;
-  const int row0 = p.offsets[t.g] + t.mt * BM;
-  const int valid = min(BM, p.offsets[t.g + 1] - row0);
   const bf16_t *Wg = (t.g < p.n_experts) ? p.W + (long long)t.g * p.w_stride : p.Ws;
 
   // Wave w fills blocks w, w + NW, ...; lane l fills row RPB b + l / CPR of its
@@ -374,17 +384,21 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void expert_gemm_wide(const GemmKA
     if (r < BM) {
       const int q = wide_slot<BK>(r, lane % CPR);
       const int rr = row0 + (r < valid ? r : 0);
-      src[i] = p.A + (long long)p.row_token[rr] * p.lda + q * 8;
+      const long long arow = GATE_UP ? (long long)p.row_token[rr] : (long long)rr;
+      src[i] = p.A + arow * p.lda + (long long)t.ks * p.kc + q * 8;
     } else {
       const int rb = r - BM;
       const int q = wide_slot<BK>(rb, lane % CPR);
-      const int wrow = (rb < BN / 2) ? t.nt * (BN / 2) + rb : p.inter + t.nt * (BN / 2) + (rb - BN / 2);
-      src[i] = Wg + (long long)wrow * p.ldw + q * 8;
+      int wrow;
+      if (GATE_UP)
+        wrow = (rb < BN / 2) ? t.nt * (BN / 2) + rb : p.inter + t.nt * (BN / 2) + (rb - BN / 2);
+      else
+        wrow = t.nt * BN + rb;
+      src[i] = Wg + (long long)wrow * p.ldw + (long long)t.ks * p.kc + q * 8;
     }
   }
   const uint32_t lds0 = lds_addr(smem);
 
-  f32x16 acc[TM][TN];
 #pragma unroll
   for (int i = 0; i < TM; ++i)
 #pragma unroll
@@ -395,14 +409,13 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void expert_gemm_wide(const GemmKA
 #pragma unroll
   for (int i = 0; i < TM; ++i) a_row[i] = wm * 128 + i * 32 + (lane & 31);
 #pragma unroll
-  for (int j = 0; j < TN; ++j) b_row[j] = j * (BN / 2) + wn * 32 + (lane & 31);
+  for (int j = 0; j < TN; ++j) b_row[j] = (GATE_UP ? j * (BN / 2) + wn * 32 : wn * 64 + j * 32) + (lane & 31);
 
-  const int KT = p.kc / BK;
-  // Stage kt (clamped to the last: loads past the end refill a buffer that is
-  // never read again) into ring buffer BUF.
+  // Stage kt (clamped to the last of the range: loads past it refill a buffer
+  // that is never read again) into ring buffer BUF.
 #define EXF_W_ISSUE(BUF, KT_)                                                                  \
   do {                                                                                         \
-    const int k0_ = min((KT_), KT - 1) * BK;                                                   \
+    const int k0_ = min((KT_), k1 - 1) * BK;                                                   \
     const uint32_t base_ = lds0 + (uint32_t)(BUF) * (STAGE * 2);                               \
     _Pragma("unroll") for (int i_ = 0; i_ < PW; ++i_)                                          \
         lds_dma16(src[i_] + k0_, base_ + (i_ * NW + wave) * 1024);                             \
@@ -424,9 +437,9 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void expert_gemm_wide(const GemmKA
             __builtin_amdgcn_mfma_f32_32x32x16_bf16(A_[i_], B_[j_], acc[i_][j_], 0, 0, 0);     \
   } while (0)
 
-  for (int q = 0; q < AHEAD; ++q) EXF_W_ISSUE(q, q);
+  for (int q = 0; q < AHEAD; ++q) EXF_W_ISSUE(q, k0 + q);
   int buf = 0;  // ring buffer of stage kt (wave-uniform)
-  for (int kt = 0; kt < KT; ++kt) {
+  for (int kt = k0; kt < k1; ++kt) {
     // Wait until this wave's loads of stage kt have landed (the later stages
     // stay in flight) and its LDS reads of the previous stage are done; after
     // the barrier every wave's part of stage kt is in LDS and nobody reads the
@@ -454,22 +467,165 @@ __global__ __launch_bounds__(64 * NW, 8 / NW) void expert_gemm_wide(const GemmKA
     }
     buf = (buf == STAGES - 1) ? 0 : buf + 1;
   }
-  // the clamped loads past the end must land before the workgroup's LDS is released
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // the clamped loads past the end land before the ring is refilled or released,
+  // and no wave still reads it
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 #undef EXF_W_ISSUE
 #undef EXF_W_FRAGS
 #undef EXF_W_MMA
+}
 
-  // ---- epilogue: H = SiLU(gate) * up ----
+// Row / column of accumulator register r of MFMA tile (i, j) of wave (wm, wn):
+// tile row 128 wm + 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4; the down column
+// (within the tile) 64 wn + 32 j + lane % 32.
+__device__ __forceinline__ int wide_row(int wm, int i, int r, int lane) {
+  return wm * 128 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+}
+
+// Finished tile: gate/up writes H = SiLU(gate) * up; down scales by the row's
+// routing weight and writes y (direct), bf16 rows Yh or fp32 rows Y.
+template <bool GATE_UP, bool DIRECT, int NW>
+__device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, int row0, int valid,
+                                           const f32x16 (&acc)[kWideTM][kWideTN]) {
+  constexpr int WN = NW / 2, BN = 64 * WN;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
 #pragma unroll
-  for (int i = 0; i < TM; ++i) {
+  for (int i = 0; i < kWideTM; ++i) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      const int ml = wm * 128 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+      const int ml = wide_row(wm, i, r, lane);
       if (ml < valid) {
-        const int n = t.nt * (BN / 2) + wn * 32 + (lane & 31);
-        p.H[(long long)(row0 + ml) * p.inter + n] = f32_to_bf16(silu(acc[i][0][r]) * acc[i][1][r]);
+        const int row = row0 + ml;
+        if (GATE_UP) {
+          const int n = t.nt * (BN / 2) + wn * 32 + (lane & 31);
+          p.H[(long long)row * p.inter + n] = f32_to_bf16(silu(acc[i][0][r]) * acc[i][1][r]);
+        } else {
+          const float w = p.row_w[row];
+#pragma unroll
+          for (int j = 0; j < kWideTN; ++j) {
+            const int n = t.nt * BN + wn * 64 + j * 32 + (lane & 31);
+            const float v = acc[i][j][r] * w;
+            if (DIRECT)
+              p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v);
+            else if (p.Yh)
+              p.Yh[(long long)row * p.d + n] = f32_to_bf16(v);
+            else
+              p.Y[((long long)t.ks * p.rows + row) * p.d + n] = v;
+          }
+        }
       }
+    }
+  }
+}
+
+template <bool GATE_UP, bool DIRECT, int BK, int STAGES, int NW>
+__global__ __launch_bounds__(64 * NW, 8 / NW) void expert_gemm_wide(const GemmKArgs p) {
+  constexpr int STAGE = (kWide + 32 * NW) * BK;
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[STAGES * STAGE];
+  TileId t;
+  if (!decode_tile(p, blockIdx.x, t)) return;
+  const int row0 = p.offsets[t.g] + t.mt * kWide;
+  const int valid = min(kWide, p.offsets[t.g + 1] - row0);
+  f32x16 acc[kWideTM][kWideTN];
+  wide_tile_mma<GATE_UP, BK, STAGES, NW>(p, t, row0, valid, 0, p.kc / BK, smem, acc);
+  wide_store<GATE_UP, DIRECT, NW>(p, t, row0, valid, acc);
+}
+
+// ---------------------------------------------------------------------------
+// Stream-K down projection on the wide tile.  Few wide tiles quantise badly
+// over the CUs (8192 Mixtral-shaped tokens give about 2.4 tiles per CU), so the
+// (tile, stage) units of all tiles are dealt out in equal contiguous ranges to
+// one workgroup per CU (ranges contiguous per XCD, in the tile order that keeps
+// the m-tiles of one weight panel together).  A workgroup's range covers at
+// least one whole tile (the planner asks for two tiles per workgroup), so a tile is
+// cut at most once: the workgroup that holds its first stages leaves the head
+// partial in P[2 lw + 1], the next one the tail partial in P[2 lw]; whole tiles
+// are stored directly.  expert_down_wide_fixup adds head + tail in that order
+// and stores those tiles.  Sums are fixed by the problem and the grid, so the
+// result is deterministic.
+// ---------------------------------------------------------------------------
+constexpr int kWideTileElems = kWide * kWide;
+
+__device__ __forceinline__ void wide_store_partial(float *P, const f32x16 (&acc)[kWideTM][kWideTN]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave >> 2, wn = wave & 3;
+#pragma unroll
+  for (int i = 0; i < kWideTM; ++i)
+#pragma unroll
+    for (int j = 0; j < kWideTN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r)
+        P[wide_row(wm, i, r, lane) * kWide + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+}
+
+__device__ __forceinline__ void sk_range(long long U, int G, int lw, long long &u0, long long &u1) {
+  u0 = U * lw / G;
+  u1 = U * (lw + 1) / G;
+}
+
+template <bool DIRECT>
+__global__ __launch_bounds__(512, 1) void expert_down_wide_sk(const GemmKArgs p) {
+  constexpr int NW = 8, BK = kWideBK, STAGES = kWideStages;
+  constexpr int STAGE = (kWide + 32 * NW) * BK;
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[STAGES * STAGE];
+  const int G = gridDim.x;
+  const int lw = xcd_remap(blockIdx.x, G);
+  const int KT = p.kc / BK;
+  const long long U = (long long)p.tile_start[p.groups] * p.n_tiles * KT;
+  long long u0, u1;
+  sk_range(U, G, lw, u0, u1);
+  for (long long u = u0; u < u1;) {
+    const int tile = (int)(u / KT), k0 = (int)(u % KT);
+    const int k1 = (int)min((long long)KT, k0 + (u1 - u));
+    TileId t;
+    tile_at(p, tile, t);
+    const int row0 = p.offsets[t.g] + t.mt * kWide;
+    const int valid = min(kWide, p.offsets[t.g + 1] - row0);
+    f32x16 acc[kWideTM][kWideTN];
+    wide_tile_mma<false, BK, STAGES, NW>(p, t, row0, valid, k0, k1, smem, acc);
+    if (k0 == 0 && k1 == KT)
+      wide_store<false, DIRECT, NW>(p, t, row0, valid, acc);
+    else
+      wide_store_partial(p.P + (size_t)(2 * lw + (k0 == 0 ? 1 : 0)) * kWideTileElems, acc);
+    u += k1 - k0;
+  }
+}
+
+// Block (b, c): the tile cut at the boundary between logical workgroups b and
+// b + 1 (if any), rows 16 c .. 16 c + 15; four columns per thread.
+template <bool DIRECT>
+__global__ __launch_bounds__(256) void expert_down_wide_fixup(const GemmKArgs p, int G) {
+  const int b = blockIdx.x + 1;
+  const int KT = p.kc / kWideBK;
+  const long long U = (long long)p.tile_start[p.groups] * p.n_tiles * KT;
+  const long long ub = U * b / G;
+  if (ub % KT == 0) return;  // no tile is cut here
+  TileId t;
+  tile_at(p, (int)(ub / KT), t);
+  const int row0 = p.offsets[t.g] + t.mt * kWide;
+  const int valid = min(kWide, p.offsets[t.g + 1] - row0);
+  const float *head = p.P + (size_t)(2 * (b - 1) + 1) * kWideTileElems;
+  const float *tail = p.P + (size_t)(2 * b) * kWideTileElems;
+  const int ml = blockIdx.y * 16 + (threadIdx.x >> 4);
+  if (ml >= valid) return;
+  const int row = row0 + ml;
+  const float w = p.row_w[row];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    const int c = q * 64 + (threadIdx.x & 15) * 4;
+    const float4 h4 = *reinterpret_cast<const float4 *>(head + ml * kWide + c);
+    const float4 t4 = *reinterpret_cast<const float4 *>(tail + ml * kWide + c);
+    const float v[4] = {(h4.x + t4.x) * w, (h4.y + t4.y) * w, (h4.z + t4.z) * w, (h4.w + t4.w) * w};
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int n = t.nt * kWide + c + e;
+      if (DIRECT)
+        p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v[e]);
+      else if (p.Yh)
+        p.Yh[(long long)row * p.d + n] = f32_to_bf16(v[e]);
+      else
+        p.Y[(long long)row * p.d + n] = v[e];
     }
   }
 }
@@ -742,9 +898,19 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
   // Few expected tiles: split the down projection's reduction so the workgroups
   // still cover every CU.  Partial sums land in separate buffers and are added
   // in a fixed order by the combine.
-  const int bm = dn_skinny ? kSkM : 128, bn = dn_skinny ? kSkN : 128;
-  const int kk = dn_skinny ? kSkK : kBK, fill = dn_skinny ? 3 : 2;
-  *dn = GemmPlan{bm, bn, 1, 0, dn_skinny ? kGemmSkinny : kGemmTile};
+  // Down projection on the wide tile, stream-K: where the gate/up projection
+  // takes it and the tiles (at least rows / 256 per 256 output columns) give
+  // every CU two whole tiles.  With fewer, the 128 x 128 tile's five or more
+  // rounds balance as well and its shorter per-tile reduction wins (measured).
+  if (!dn_skinny && gu_wide && d % kWide == 0 && (long long)(rows / kWide) * (d / kWide) >= 2LL * cu_count) {
+    *dn = GemmPlan{kWide, kWide, 1, cu_count, kGemmWideSK};
+    return;
+  }
+  const bool dn_wide = kWideDown && !dn_skinny && gu_wide && d % (32 * kWideWaves) == 0;
+  const int bm = dn_skinny ? kSkM : dn_wide ? kWide : 128;
+  const int bn = dn_skinny ? kSkN : dn_wide ? 32 * kWideWaves : 128;
+  const int kk = dn_skinny ? kSkK : kBK, fill = dn_skinny ? 3 : dn_wide ? 0 : 2;
+  *dn = GemmPlan{bm, bn, 1, 0, dn_skinny ? kGemmSkinny : dn_wide ? kGemmWide : kGemmTile};
   const int mt_expect = (rows + bm - 1) / bm > active ? (rows + bm - 1) / bm : active;
   const int dn_tiles = mt_expect * (d / bn);
   if (dn_tiles < fill * cu_count) {
@@ -818,13 +984,31 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
     if (gu.kind == kGemmSkinny)
       expert_gemm_skinny<true, false><<<gu.grid, 256, 0, s>>>(ga);
     else if (gu.kind == kGemmWide)
-      expert_gemm_wide<kWideBK, kWideStages, kWideWaves><<<gu.grid, 64 * kWideWaves, 0, s>>>(ga);
+      expert_gemm_wide<true, false, kWideBK, kWideStages, kWideWaves><<<gu.grid, 64 * kWideWaves, 0, s>>>(ga);
     else
       expert_gemm_tile<128, 128, 2, true, false><<<gu.grid, 256, 0, s>>>(ga);
   }
   if (ev_mid) (void)hipEventRecord(ev_mid, s);
   if (dn.grid > 0) {
-    if (dn.kind == kGemmSkinny) {
+    if (dn.kind == kGemmWideSK) {
+      da.P = a.skp;
+      if (a.direct)
+        expert_down_wide_sk<true><<<dn.grid, 512, 0, s>>>(da);
+      else
+        expert_down_wide_sk<false><<<dn.grid, 512, 0, s>>>(da);
+      if (dn.grid > 1) {
+        const dim3 fg(dn.grid - 1, kWide / 16);
+        if (a.direct)
+          expert_down_wide_fixup<true><<<fg, 256, 0, s>>>(da, dn.grid);
+        else
+          expert_down_wide_fixup<false><<<fg, 256, 0, s>>>(da, dn.grid);
+      }
+    } else if (dn.kind == kGemmWide) {
+      if (a.direct)
+        expert_gemm_wide<false, true, kWideBK, kWideStages, kWideWaves><<<dn.grid, 64 * kWideWaves, 0, s>>>(da);
+      else
+        expert_gemm_wide<false, false, kWideBK, kWideStages, kWideWaves><<<dn.grid, 64 * kWideWaves, 0, s>>>(da);
+    } else if (dn.kind == kGemmSkinny) {
       if (a.direct)
         expert_gemm_skinny<false, true><<<dn.grid, 256, 0, s>>>(da);
       else

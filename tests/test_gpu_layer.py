@@ -248,3 +248,32 @@ def test_execute_every_kernel_path(shape_name, T, k_out):
     ref = O.moe_output(lp.ref, synth.widen(xs), ids, w)
     err = per_token_rel_l2(from_dev(y), ref)
     assert err.max() <= TOL_Y["bf16"], err.max()
+
+
+# Enough wide tiles for two per CU on 256 CUs: the down projection takes the
+# stream-K path (tile stages dealt out evenly; a tile cut between two
+# workgroups is finished by the fixup kernel).
+SK_SHAPE = synth.LayerShape("stream-k", d=2048, inter=512, n_experts=8, top_k=2, dtype="bf16")
+
+
+@pytest.mark.parametrize("T,k_out", [(16384, 1), (8192, 2), (20000, 1)])
+def test_execute_stream_k_down(T, k_out):
+    shape = SK_SHAPE
+    lp = LayerPair(shape, seed=13)
+    rng = np.random.default_rng(T + k_out)
+    p = np.array([0.22, 0.18, 0.15, 0.13, 0.12, 0.1, 0.06, 0.04])
+    ids = rng.choice(shape.n_experts, size=(T, k_out), p=p).astype(np.int32)
+    if k_out == 2:   # two distinct routes per token
+        ids[:, 1] = np.where(ids[:, 1] == ids[:, 0], (ids[:, 0] + 1) % shape.n_experts, ids[:, 1])
+    w = rng.standard_normal((T, k_out)).astype(np.float32)
+    xs = synth.tokens(shape, T, seed=13)
+    y = from_dev(X.moe_execute(lp.dev, to_dev(xs), to_dev(ids), to_dev(w)))
+    sync()
+    smp = np.sort(np.concatenate([[0, T - 1], rng.choice(np.arange(1, T - 1), 254, replace=False)]))
+    ref = O.moe_output(lp.ref, synth.widen(xs[smp]), ids[smp], w[smp])
+    err = per_token_rel_l2(y[smp], ref)
+    assert err.max() <= TOL_Y["bf16"], err.max()
+    # every token of the batch was written (a tile missed by the fixup would leave garbage or zeros)
+    assert np.isfinite(y).all()
+    norms = np.linalg.norm(y, axis=1)
+    assert (norms > 0).all()
