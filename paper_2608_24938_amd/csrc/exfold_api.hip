@@ -75,7 +75,7 @@ struct ExecPlan {
   bool direct = false;
   GemmPlan gu{}, dn{};
   size_t o_blk = 0, o_offsets = 0, o_ts0 = 0, o_ts1 = 0, o_row_token = 0, o_row_slot = 0,
-         o_row_w = 0, o_slot_row = 0, o_H = 0, o_Y = 0, o_skp = 0;
+         o_row_w = 0, o_slot_row = 0, o_H = 0, o_Y = 0, o_wpart = 0;
 };
 
 void plan_exec(const exfold_layer *L, int phase, int T, int k_out, bool with_shared,
@@ -110,7 +110,11 @@ void plan_exec(const exfold_layer *L, int phase, int T, int k_out, bool with_sha
     p.dn.ksplit = 1;
   }
   p.o_Y = p.direct ? c.take(0) : c.take(sizeof(float) * (size_t)p.dn.ksplit * p.rows * p.d);
-  p.o_skp = c.take(p.dn.kind == kGemmWideSK ? sizeof(float) * wide_sk_partial_floats(p.dn.grid) : 0);
+  {
+    const int wg = p.gu.kind == kGemmWide ? p.gu.wgs : 0, wd = p.dn.kind == kGemmWide ? p.dn.wgs : 0;
+    const int wgs = wg > wd ? wg : wd;
+    p.o_wpart = c.take(sizeof(float) * wide_partial_floats(wgs));  // shared: the GEMMs run in order
+  }
 }
 
 template <typename T> T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
@@ -168,7 +172,7 @@ exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
   // rows that only the combine reads travel as bf16 (each term rounded once
   // before the fp32 sum over the token's routes); kept rows stay fp32
   a.y_bf16 = p.dtype == EXFOLD_BF16 && !p.direct && !keep_rows && p.dn.ksplit == 1;
-  a.skp = at<float>(ws, p.o_skp);
+  a.wide_part = at<float>(ws, p.o_wpart);
   hipEvent_t ev_mid = (events && events[EXFOLD_EV_GATE_UP])
                           ? static_cast<hipEvent_t>(events[EXFOLD_EV_GATE_UP]) : nullptr;
   if (launch_expert_gemms(a, p.gu, p.dn, s, ev_mid) != hipSuccess) return EXFOLD_ERR_DEVICE;

@@ -36,7 +36,7 @@ struct GemmKArgs {
   bf16_t *H;
   float *Y;
   bf16_t *Yh;  // down, when set: bf16 per-row outputs instead of Y (no split)
-  float *P;    // down, stream-K: partial tiles [2 * workgroups][256 * 256]
+  float *P;    // wide tiles: split-remainder partial tiles [workgroups][256 * 256]
   bf16_t *y;
   const float *row_w;
 };
@@ -316,7 +316,6 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
 // buffers (more bytes in flight, but 64-byte row pieces and twice the barriers).
 // ---------------------------------------------------------------------------
 constexpr int kWide = 256, kWideWaves = 8, kWideBK = 64, kWideStages = 2;
-constexpr bool kWideDown = false;
 
 // LDS byte address of a shared-memory pointer (for M0).
 __device__ __forceinline__ uint32_t lds_addr(const void *ptr) {
@@ -519,33 +518,37 @@ __device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, 
   }
 }
 
-template <bool GATE_UP, bool DIRECT, int BK, int STAGES, int NW>
-__global__ __launch_bounds__(64 * NW, 8 / NW) void expert_gemm_wide(const GemmKArgs p) {
-  constexpr int STAGE = (kWide + 32 * NW) * BK;
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[STAGES * STAGE];
-  TileId t;
-  if (!decode_tile(p, blockIdx.x, t)) return;
-  const int row0 = p.offsets[t.g] + t.mt * kWide;
-  const int valid = min(kWide, p.offsets[t.g + 1] - row0);
-  f32x16 acc[kWideTM][kWideTN];
-  wide_tile_mma<GATE_UP, BK, STAGES, NW>(p, t, row0, valid, 0, p.kc / BK, smem, acc);
-  wide_store<GATE_UP, DIRECT, NW>(p, t, row0, valid, acc);
-}
-
 // ---------------------------------------------------------------------------
-// Stream-K down projection on the wide tile.  Few wide tiles quantise badly
-// over the CUs (8192 Mixtral-shaped tokens give about 2.4 tiles per CU), so the
-// (tile, stage) units of all tiles are dealt out in equal contiguous ranges to
-// one workgroup per CU (ranges contiguous per XCD, in the tile order that keeps
-// the m-tiles of one weight panel together).  A workgroup's range covers at
-// least one whole tile (the planner asks for two tiles per workgroup), so a tile is
-// cut at most once: the workgroup that holds its first stages leaves the head
-// partial in P[2 lw + 1], the next one the tail partial in P[2 lw]; whole tiles
-// are stored directly.  expert_down_wide_fixup adds head + tail in that order
-// and stores those tiles.  Sums are fixed by the problem and the grid, so the
-// result is deterministic.
+// Wide-tile launches: whole rounds of tiles plus a split remainder.  With one
+// workgroup per CU (the ring takes 128 KiB of LDS), tiles run in rounds of G =
+// CU count; the last, partial round would leave most CUs idle.  When it holds
+// at most half a round, its rem tiles have their reductions cut into s equal
+// ranges of stages (s = G / rem, at most kWideMaxSplit, at least four stages a
+// range) on separate workgroups: range c of remainder tile r leaves its fp32
+// partial tile in P[r s + c], and expert_wide_fixup adds the s partials in
+// range order and applies the epilogue.  Whole tiles keep the lock-step order
+// in which the m-tiles of one weight panel and the n-tiles of one row block
+// share an XCD's L2 (dealing the stages of every tile out evenly instead
+// breaks that sharing: measured slower).  The ranges of one remainder tile are
+// disjoint in K, so the remainder is laid out range-major: neighbouring
+// workgroups take neighbouring tiles over the same stages.  The sums depend on
+// the problem and G only, so the result is deterministic.
 // ---------------------------------------------------------------------------
 constexpr int kWideTileElems = kWide * kWide;
+constexpr int kWideMaxSplit = 16;
+
+struct WideSplit {
+  int ndp;  // tiles run whole: logical ids 0 .. ndp - 1
+  int rem;  // tiles split s ways: logical ids ndp .. ndp + rem - 1
+  int s;
+};
+__device__ __forceinline__ WideSplit wide_split(const GemmKArgs &p, int G) {
+  const int total = p.tile_start[p.groups] * p.n_tiles;
+  const int rem = total % G;
+  const int s = rem > 0 ? min(G / rem, min(kWideMaxSplit, p.kc / kWideBK / 4)) : 1;
+  if (rem > 0 && s >= 2) return WideSplit{total - rem, rem, s};
+  return WideSplit{total, 0, 1};
+}
 
 __device__ __forceinline__ void wide_store_partial(float *P, const f32x16 (&acc)[kWideTM][kWideTN]) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -559,73 +562,106 @@ __device__ __forceinline__ void wide_store_partial(float *P, const f32x16 (&acc)
         P[wide_row(wm, i, r, lane) * kWide + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
 }
 
-__device__ __forceinline__ void sk_range(long long U, int G, int lw, long long &u0, long long &u1) {
-  u0 = U * lw / G;
-  u1 = U * (lw + 1) / G;
-}
-
-template <bool DIRECT>
-__global__ __launch_bounds__(512, 1) void expert_down_wide_sk(const GemmKArgs p) {
-  constexpr int NW = 8, BK = kWideBK, STAGES = kWideStages;
-  constexpr int STAGE = (kWide + 32 * NW) * BK;
-  __shared__ __attribute__((aligned(1024))) bf16_t smem[STAGES * STAGE];
-  const int G = gridDim.x;
-  const int lw = xcd_remap(blockIdx.x, G);
-  const int KT = p.kc / BK;
-  const long long U = (long long)p.tile_start[p.groups] * p.n_tiles * KT;
-  long long u0, u1;
-  sk_range(U, G, lw, u0, u1);
-  for (long long u = u0; u < u1;) {
-    const int tile = (int)(u / KT), k0 = (int)(u % KT);
-    const int k1 = (int)min((long long)KT, k0 + (u1 - u));
-    TileId t;
-    tile_at(p, tile, t);
-    const int row0 = p.offsets[t.g] + t.mt * kWide;
-    const int valid = min(kWide, p.offsets[t.g + 1] - row0);
-    f32x16 acc[kWideTM][kWideTN];
-    wide_tile_mma<false, BK, STAGES, NW>(p, t, row0, valid, k0, k1, smem, acc);
-    if (k0 == 0 && k1 == KT)
-      wide_store<false, DIRECT, NW>(p, t, row0, valid, acc);
-    else
-      wide_store_partial(p.P + (size_t)(2 * lw + (k0 == 0 ? 1 : 0)) * kWideTileElems, acc);
-    u += k1 - k0;
-  }
-}
-
-// Block (b, c): the tile cut at the boundary between logical workgroups b and
-// b + 1 (if any), rows 16 c .. 16 c + 15; four columns per thread.
-template <bool DIRECT>
-__global__ __launch_bounds__(256) void expert_down_wide_fixup(const GemmKArgs p, int G) {
-  const int b = blockIdx.x + 1;
+// Workgroup blockIdx.x of a launch of ndp + rem s workgroups (more exit).
+template <bool GATE_UP, bool DIRECT>
+__device__ __forceinline__ void wide_gemm(const GemmKArgs &p, int G, bf16_t *smem) {
+  constexpr int NW = kWideWaves;
+  const WideSplit w = wide_split(p, G);
   const int KT = p.kc / kWideBK;
-  const long long U = (long long)p.tile_start[p.groups] * p.n_tiles * KT;
-  const long long ub = U * b / G;
-  if (ub % KT == 0) return;  // no tile is cut here
+  const int b = blockIdx.x;
   TileId t;
-  tile_at(p, (int)(ub / KT), t);
+  int k0 = 0, k1 = KT;
+  float *part = nullptr;
+  if (b < w.ndp) {
+    tile_at(p, xcd_remap(b, w.ndp), t);
+  } else {
+    const int j = b - w.ndp, n = w.rem * w.s;
+    if (j >= n) return;
+    const int lj = xcd_remap(j, n), c = lj / w.rem, r = lj % w.rem;
+    tile_at(p, w.ndp + r, t);
+    k0 = c * KT / w.s;
+    k1 = (c + 1) * KT / w.s;
+    part = p.P + (size_t)(r * w.s + c) * kWideTileElems;
+  }
   const int row0 = p.offsets[t.g] + t.mt * kWide;
   const int valid = min(kWide, p.offsets[t.g + 1] - row0);
-  const float *head = p.P + (size_t)(2 * (b - 1) + 1) * kWideTileElems;
-  const float *tail = p.P + (size_t)(2 * b) * kWideTileElems;
+  f32x16 acc[kWideTM][kWideTN];
+  wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW>(p, t, row0, valid, k0, k1, smem, acc);
+  if (part)
+    wide_store_partial(part, acc);
+  else
+    wide_store<GATE_UP, DIRECT, NW>(p, t, row0, valid, acc);
+}
+
+constexpr int kWideSmemElems = kWideStages * (kWide + 32 * kWideWaves) * kWideBK;
+
+__global__ __launch_bounds__(64 * kWideWaves, 1) void expert_gate_up_wide(const GemmKArgs p, int G) {
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[kWideSmemElems];
+  wide_gemm<true, false>(p, G, smem);
+}
+
+template <bool DIRECT>
+__global__ __launch_bounds__(64 * kWideWaves, 1) void expert_down_wide(const GemmKArgs p, int G) {
+  __shared__ __attribute__((aligned(1024))) bf16_t smem[kWideSmemElems];
+  wide_gemm<false, DIRECT>(p, G, smem);
+}
+
+// Block (r, c): remainder tile r, tile rows 16 c .. 16 c + 15, sixteen threads
+// a row.  Gate/up: H columns 128 nt + col from the gate partials (column
+// 64 (col / 32) + col % 32) and the up partials 32 columns further; down: the
+// 256 output columns scaled by the row's routing weight.
+template <bool GATE_UP, bool DIRECT>
+__global__ __launch_bounds__(256) void expert_wide_fixup(const GemmKArgs p, int G) {
+  const WideSplit w = wide_split(p, G);
+  const int r = blockIdx.x;
+  if (r >= w.rem) return;
+  TileId t;
+  tile_at(p, w.ndp + r, t);
+  const int row0 = p.offsets[t.g] + t.mt * kWide;
+  const int valid = min(kWide, p.offsets[t.g + 1] - row0);
   const int ml = blockIdx.y * 16 + (threadIdx.x >> 4);
   if (ml >= valid) return;
   const int row = row0 + ml;
-  const float w = p.row_w[row];
+  const float *P0 = p.P + (size_t)r * w.s * kWideTileElems + (size_t)ml * kWide;
+  auto sum4 = [&](int col) {
+    float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
+    for (int k = 0; k < w.s; ++k) {
+      const float4 q = *reinterpret_cast<const float4 *>(P0 + (size_t)k * kWideTileElems + col);
+      v.x += q.x;
+      v.y += q.y;
+      v.z += q.z;
+      v.w += q.w;
+    }
+    return v;
+  };
+  if (GATE_UP) {
 #pragma unroll
-  for (int q = 0; q < 4; ++q) {
-    const int c = q * 64 + (threadIdx.x & 15) * 4;
-    const float4 h4 = *reinterpret_cast<const float4 *>(head + ml * kWide + c);
-    const float4 t4 = *reinterpret_cast<const float4 *>(tail + ml * kWide + c);
-    const float v[4] = {(h4.x + t4.x) * w, (h4.y + t4.y) * w, (h4.z + t4.z) * w, (h4.w + t4.w) * w};
+    for (int q = 0; q < 2; ++q) {
+      const int col = q * 64 + (threadIdx.x & 15) * 4;
+      const int pc = (col >> 5) * 64 + (col & 31);
+      const float4 g = sum4(pc), u = sum4(pc + 32);
+      const float h[4] = {silu(g.x) * u.x, silu(g.y) * u.y, silu(g.z) * u.z, silu(g.w) * u.w};
+      bf16_t *dst = p.H + (long long)row * p.inter + t.nt * (kWide / 2) + col;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const int n = t.nt * kWide + c + e;
-      if (DIRECT)
-        p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v[e]);
-      else if (p.Yh)
-        p.Yh[(long long)row * p.d + n] = f32_to_bf16(v[e]);
-      else
-        p.Y[(long long)row * p.d + n] = v[e];
+      for (int e = 0; e < 4; ++e) dst[e] = f32_to_bf16(h[e]);
+    }
+  } else {
+    const float rw = p.row_w[row];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int col = q * 64 + (threadIdx.x & 15) * 4;
+      const float4 a = sum4(col);
+      const float v[4] = {a.x * rw, a.y * rw, a.z * rw, a.w * rw};
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int n = t.nt * kWide + col + e;
+        if (DIRECT)
+          p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v[e]);
+        else if (p.Yh)
+          p.Yh[(long long)row * p.d + n] = f32_to_bf16(v[e]);
+        else
+          p.Y[(long long)row * p.d + n] = v[e];
+      }
     }
   }
 }
@@ -889,28 +925,27 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
     *gu = GemmPlan{kSkM, kSkN, 1, 0, kGemmSkinny};
     gu->grid = (rows / kSkM + groups) * (inter / (kSkN / 2));  // >= sum of ceil(rows_g / 32) tiles
   } else if (gu_wide) {
-    *gu = GemmPlan{kWide, 64 * (kWideWaves / 2), 1, 0, kGemmWide};
-    gu->grid = (rows / kWide + groups) * (inter / (32 * (kWideWaves / 2)));
+    // whole rounds plus the split remainder: at most ceil tiles + one round
+    *gu = GemmPlan{kWide, 64 * (kWideWaves / 2), 1, 0, kGemmWide, cu_count};
+    gu->grid = (rows / kWide + groups) * (inter / (32 * (kWideWaves / 2))) + cu_count;
   } else {
     *gu = GemmPlan{128, 128, 1, 0, kGemmTile};
     gu->grid = (rows / 128 + groups) * (inter / 64);
   }
+  // Down projection on the wide tile where the gate/up projection takes it and
+  // the tiles (at least rows / 256 per 256 output columns) fill one round.
+  if (!dn_skinny && gu_wide && d % kWide == 0 && (long long)(rows / kWide) * (d / kWide) >= cu_count) {
+    *dn = GemmPlan{kWide, kWide, 1, 0, kGemmWide, cu_count};
+    dn->grid = (rows / kWide + groups) * (d / kWide) + cu_count;
+    return;
+  }
   // Few expected tiles: split the down projection's reduction so the workgroups
   // still cover every CU.  Partial sums land in separate buffers and are added
   // in a fixed order by the combine.
-  // Down projection on the wide tile, stream-K: where the gate/up projection
-  // takes it and the tiles (at least rows / 256 per 256 output columns) give
-  // every CU two whole tiles.  With fewer, the 128 x 128 tile's five or more
-  // rounds balance as well and its shorter per-tile reduction wins (measured).
-  if (!dn_skinny && gu_wide && d % kWide == 0 && (long long)(rows / kWide) * (d / kWide) >= 2LL * cu_count) {
-    *dn = GemmPlan{kWide, kWide, 1, cu_count, kGemmWideSK};
-    return;
-  }
-  const bool dn_wide = kWideDown && !dn_skinny && gu_wide && d % (32 * kWideWaves) == 0;
-  const int bm = dn_skinny ? kSkM : dn_wide ? kWide : 128;
-  const int bn = dn_skinny ? kSkN : dn_wide ? 32 * kWideWaves : 128;
-  const int kk = dn_skinny ? kSkK : kBK, fill = dn_skinny ? 3 : dn_wide ? 0 : 2;
-  *dn = GemmPlan{bm, bn, 1, 0, dn_skinny ? kGemmSkinny : dn_wide ? kGemmWide : kGemmTile};
+  const int bm = dn_skinny ? kSkM : 128;
+  const int bn = dn_skinny ? kSkN : 128;
+  const int kk = dn_skinny ? kSkK : kBK, fill = dn_skinny ? 3 : 2;
+  *dn = GemmPlan{bm, bn, 1, 0, dn_skinny ? kGemmSkinny : kGemmTile};
   const int mt_expect = (rows + bm - 1) / bm > active ? (rows + bm - 1) / bm : active;
   const int dn_tiles = mt_expect * (d / bn);
   if (dn_tiles < fill * cu_count) {
@@ -981,33 +1016,28 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
   da.row_w = a.row_w;
 
   if (gu.grid > 0) {
-    if (gu.kind == kGemmSkinny)
+    if (gu.kind == kGemmSkinny) {
       expert_gemm_skinny<true, false><<<gu.grid, 256, 0, s>>>(ga);
-    else if (gu.kind == kGemmWide)
-      expert_gemm_wide<true, false, kWideBK, kWideStages, kWideWaves><<<gu.grid, 64 * kWideWaves, 0, s>>>(ga);
-    else
+    } else if (gu.kind == kGemmWide) {
+      ga.P = a.wide_part;
+      expert_gate_up_wide<<<gu.grid, 64 * kWideWaves, 0, s>>>(ga, gu.wgs);
+      expert_wide_fixup<true, false><<<dim3(gu.wgs / 2, kWide / 16), 256, 0, s>>>(ga, gu.wgs);
+    } else {
       expert_gemm_tile<128, 128, 2, true, false><<<gu.grid, 256, 0, s>>>(ga);
+    }
   }
   if (ev_mid) (void)hipEventRecord(ev_mid, s);
   if (dn.grid > 0) {
-    if (dn.kind == kGemmWideSK) {
-      da.P = a.skp;
-      if (a.direct)
-        expert_down_wide_sk<true><<<dn.grid, 512, 0, s>>>(da);
-      else
-        expert_down_wide_sk<false><<<dn.grid, 512, 0, s>>>(da);
-      if (dn.grid > 1) {
-        const dim3 fg(dn.grid - 1, kWide / 16);
-        if (a.direct)
-          expert_down_wide_fixup<true><<<fg, 256, 0, s>>>(da, dn.grid);
-        else
-          expert_down_wide_fixup<false><<<fg, 256, 0, s>>>(da, dn.grid);
+    if (dn.kind == kGemmWide) {
+      da.P = a.wide_part;
+      const dim3 fg(dn.wgs / 2, kWide / 16);
+      if (a.direct) {
+        expert_down_wide<true><<<dn.grid, 64 * kWideWaves, 0, s>>>(da, dn.wgs);
+        expert_wide_fixup<false, true><<<fg, 256, 0, s>>>(da, dn.wgs);
+      } else {
+        expert_down_wide<false><<<dn.grid, 64 * kWideWaves, 0, s>>>(da, dn.wgs);
+        expert_wide_fixup<false, false><<<fg, 256, 0, s>>>(da, dn.wgs);
       }
-    } else if (dn.kind == kGemmWide) {
-      if (a.direct)
-        expert_gemm_wide<false, true, kWideBK, kWideStages, kWideWaves><<<dn.grid, 64 * kWideWaves, 0, s>>>(da);
-      else
-        expert_gemm_wide<false, false, kWideBK, kWideStages, kWideWaves><<<dn.grid, 64 * kWideWaves, 0, s>>>(da);
     } else if (dn.kind == kGemmSkinny) {
       if (a.direct)
         expert_gemm_skinny<false, true><<<dn.grid, 256, 0, s>>>(da);

@@ -67,14 +67,15 @@ hipError_t launch_static_pool(const float *h, int N, int D, const float *S, cons
 
 // ---- expert GEMMs and combine (k_gemm.hip) ----
 // kGemmTile: 128x128 tiles; kGemmSkinny: 32x64 tiles for few rows per expert;
-// kGemmWide: 256x256 tiles (eight waves, loads straight into LDS); kGemmWideSK:
-// the same tile for the down projection with its stages dealt out stream-K.
-enum { kGemmSimt = 0, kGemmTile = 1, kGemmSkinny = 2, kGemmWide = 3, kGemmWideSK = 4 };
+// kGemmWide: 256x256 tiles (eight waves, loads straight into LDS) in rounds of
+// `wgs` workgroups, a short last round split along the reduction.
+enum { kGemmSimt = 0, kGemmTile = 1, kGemmSkinny = 2, kGemmWide = 3 };
 struct GemmPlan {
   int bm, bn;  // tile height (rows) and width (output columns, or weight rows for gate/up)
   int ksplit;  // splits of the reduction (down projection only; partial outputs)
   int grid;    // workgroups launched (an upper bound on the device-side tile count)
   int kind;    // kGemmSimt (float32 layers), kGemmTile, kGemmSkinny or kGemmWide (bf16 MFMA tiles)
+  int wgs;     // kGemmWide: workgroups per round (one per CU)
 };
 struct ExpertArgs {
   int dtype;
@@ -91,10 +92,11 @@ struct ExpertArgs {
   void *y;      // [T, d] direct output (each token owns exactly one row)
   bool direct;
   bool y_bf16;  // bf16 GEMMs, no split: Y holds [rows, d] bf16 rows instead
-  float *skp;   // stream-K down: partial tiles, wide_sk_partial_floats(grid) floats
+  float *wide_part;  // kGemmWide: split-remainder partial tiles, wide_partial_floats(wgs) floats
 };
-// Partial-tile scratch of the stream-K down projection on `grid` workgroups.
-inline size_t wide_sk_partial_floats(int grid) { return (size_t)2 * grid * 256 * 256; }
+// Partial-tile scratch of a kGemmWide launch in rounds of `wgs` workgroups (the
+// split remainder holds at most wgs partial 256x256 tiles).
+inline size_t wide_partial_floats(int wgs) { return (size_t)wgs * 256 * 256; }
 // active_groups: expected number of non-empty groups (sizes the down split).
 void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d, int inter,
                        int cu_count, GemmPlan *gate_up, GemmPlan *down);

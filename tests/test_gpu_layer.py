@@ -250,30 +250,60 @@ def test_execute_every_kernel_path(shape_name, T, k_out):
     assert err.max() <= TOL_Y["bf16"], err.max()
 
 
-# Enough wide tiles for two per CU on 256 CUs: the down projection takes the
-# stream-K path (tile stages dealt out evenly; a tile cut between two
-# workgroups is finished by the fixup kernel).
-SK_SHAPE = synth.LayerShape("stream-k", d=2048, inter=512, n_experts=8, top_k=2, dtype="bf16")
+# Wide 256x256 tiles for both GEMMs (2 rows >= 3 x 256 per expert and at
+# least one round of down tiles): whole rounds of one tile per CU, then a short
+# last round whose tiles are split along the reduction and finished by the
+# fixup kernel.
+SPLIT_SHAPE = synth.LayerShape("wide-split", d=2048, inter=1024, n_experts=8, top_k=2, dtype="bf16")
 
 
-@pytest.mark.parametrize("T,k_out", [(16384, 1), (8192, 2), (20000, 1)])
-def test_execute_stream_k_down(T, k_out):
-    shape = SK_SHAPE
-    lp = LayerPair(shape, seed=13)
-    rng = np.random.default_rng(T + k_out)
-    p = np.array([0.22, 0.18, 0.15, 0.13, 0.12, 0.1, 0.06, 0.04])
-    ids = rng.choice(shape.n_experts, size=(T, k_out), p=p).astype(np.int32)
-    if k_out == 2:   # two distinct routes per token
-        ids[:, 1] = np.where(ids[:, 1] == ids[:, 0], (ids[:, 0] + 1) % shape.n_experts, ids[:, 1])
+def _routes_with_counts(counts, k_out, rng):
+    """[T, k_out] routes in which expert e appears counts[e] times, distinct within a token."""
+    labels = np.repeat(np.arange(len(counts)), counts).astype(np.int32)
+    T = labels.size // k_out
+    ids = labels.reshape(k_out, T).T.copy()   # every block of one label is shorter than T
+    return ids[rng.permutation(T)]
+
+
+def _wide_split(tiles, G):
+    """(whole tiles, remainder tiles, split) of a wide launch of `tiles` tiles in rounds of G."""
+    rem = tiles % G
+    return (tiles - rem, rem, G // rem) if rem and 2 * rem <= G else (tiles, 0, 1)
+
+
+# counts -> m-tiles of 256 rows: 38 (both GEMMs 304 tiles: 48 split 5 / 4 ways),
+# 48 (384 tiles: 128 split twice, the largest split remainder) and 50 (400
+# tiles: 144 left whole)
+SPLIT_COUNTS = {38: [1300, 1200, 1100, 1000, 1400, 1000, 1000, 1000],
+                48: [1500, 1500, 1536, 1537, 1200, 1300, 1400, 1300],
+                50: [1500, 1500, 1536, 1538, 1290, 1300, 1400, 1540]}
+
+
+@pytest.mark.parametrize("mtiles,k_out", [(38, 1), (38, 2), (48, 1), (50, 2)])
+def test_execute_wide_split_remainder(mtiles, k_out):
+    shape = SPLIT_SHAPE
+    counts = np.array(SPLIT_COUNTS[mtiles])
+    assert int(np.ceil(counts / 256).sum()) == mtiles
+    G = torch.cuda.get_device_properties(0).multi_processor_count
+    tiles = mtiles * (shape.d // 256)          # = mtiles * (inter // 128) for the gate/up GEMM
+    print(f"wide split: {mtiles} m-tiles, k_out={k_out}, G={G}: whole/rem/split {_wide_split(tiles, G)}",
+          flush=True)
+    lp = LayerPair(shape, seed=17)
+    rng = np.random.default_rng(mtiles * 10 + k_out)
+    ids = _routes_with_counts(counts, k_out, rng)
+    T = ids.shape[0]
     w = rng.standard_normal((T, k_out)).astype(np.float32)
-    xs = synth.tokens(shape, T, seed=13)
+    xs = synth.tokens(shape, T, seed=17)
     y = from_dev(X.moe_execute(lp.dev, to_dev(xs), to_dev(ids), to_dev(w)))
     sync()
     smp = np.sort(np.concatenate([[0, T - 1], rng.choice(np.arange(1, T - 1), 254, replace=False)]))
     ref = O.moe_output(lp.ref, synth.widen(xs[smp]), ids[smp], w[smp])
     err = per_token_rel_l2(y[smp], ref)
     assert err.max() <= TOL_Y["bf16"], err.max()
-    # every token of the batch was written (a tile missed by the fixup would leave garbage or zeros)
+    # every token was written: a tile left out of the fixup would leave stale or zero rows
     assert np.isfinite(y).all()
-    norms = np.linalg.norm(y, axis=1)
-    assert (norms > 0).all()
+    assert (np.linalg.norm(y, axis=1) > 0).all()
+    # the result does not depend on the run (fixed summation order of the split partials)
+    y2 = from_dev(X.moe_execute(lp.dev, to_dev(xs), to_dev(ids), to_dev(w)))
+    sync()
+    np.testing.assert_array_equal(y, y2)
