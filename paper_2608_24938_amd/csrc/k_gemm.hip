@@ -347,8 +347,10 @@ constexpr int kWideTM = 4, kWideTN = 2;  // 32x32 MFMA tiles per wave
 // Main loop of one wide tile over the reduction stages [k0, k1): zeroes acc,
 // streams the stages through the LDS ring and leaves the products in acc.
 // All waves of the workgroup call it; it ends with every load landed and a
-// barrier, so the ring may be refilled right after.
-template <bool GATE_UP, int BK, int STAGES, int NW>
+// barrier, so the ring may be refilled right after.  HALF (a group's last
+// tile holding at most 128 rows): the A rows 128..255 are not loaded and the
+// waves owning them skip their MFMAs (their accumulators stay zero).
+template <bool GATE_UP, int BK, int STAGES, int NW, bool HALF>
 __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &t, int row0, int valid,
                                               int k0, int k1, bf16_t *smem,
                                               f32x16 (&acc)[kWideTM][kWideTN]) {
@@ -365,6 +367,8 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
   constexpr int VMC = (AHEAD - 1) * PW;          // loads allowed in flight at a stage's wait
   static_assert(VMC == 0 || VMC == 6 || VMC == 8 || VMC == 12 || VMC == 16, "vmcnt immediates below");
   static_assert(BLOCKS % NW == 0, "blocks per wave");
+  static_assert(!HALF || VMC == 0, "HALF issues fewer loads per stage: one stage in flight only");
+  static_assert((NW * RPB) % (BM / 2) == 0 || (BM / 2) % (NW * RPB) == 0, "A halves by load index");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -417,7 +421,8 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
     const int k0_ = min((KT_), k1 - 1) * BK;                                                   \
     const uint32_t base_ = lds0 + (uint32_t)(BUF) * (STAGE * 2);                               \
     _Pragma("unroll") for (int i_ = 0; i_ < PW; ++i_)                                          \
-        lds_dma16(src[i_] + k0_, base_ + (i_ * NW + wave) * 1024);                             \
+        if (!HALF || i_ * NW * RPB < BM / 2 || i_ * NW * RPB >= BM)                            \
+            lds_dma16(src[i_] + k0_, base_ + (i_ * NW + wave) * 1024);                         \
   } while (0)
 #define EXF_W_FRAGS(A_, B_, BUF, S_)                                                           \
   do {                                                                                         \
@@ -456,13 +461,15 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
       asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     const int prev = (buf == 0) ? STAGES - 1 : buf - 1;
     EXF_W_ISSUE(prev, kt + AHEAD);
+    if (!HALF || wm == 0) {
 #pragma unroll
-    for (int s2 = 0; s2 < BK / 32; ++s2) {
-      bf16x8 a0_[TM], b0_[TN], a1_[TM], b1_[TN];
-      EXF_W_FRAGS(a0_, b0_, buf, 2 * s2);
-      EXF_W_FRAGS(a1_, b1_, buf, 2 * s2 + 1);
-      EXF_W_MMA(a0_, b0_);
-      EXF_W_MMA(a1_, b1_);
+      for (int s2 = 0; s2 < BK / 32; ++s2) {
+        bf16x8 a0_[TM], b0_[TN], a1_[TM], b1_[TN];
+        EXF_W_FRAGS(a0_, b0_, buf, 2 * s2);
+        EXF_W_FRAGS(a1_, b1_, buf, 2 * s2 + 1);
+        EXF_W_MMA(a0_, b0_);
+        EXF_W_MMA(a1_, b1_);
+      }
     }
     buf = (buf == STAGES - 1) ? 0 : buf + 1;
   }
@@ -586,7 +593,10 @@ __device__ __forceinline__ void wide_gemm(const GemmKArgs &p, int G, bf16_t *sme
   const int row0 = p.offsets[t.g] + t.mt * kWide;
   const int valid = min(kWide, p.offsets[t.g + 1] - row0);
   f32x16 acc[kWideTM][kWideTN];
-  wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW>(p, t, row0, valid, k0, k1, smem, acc);
+  if (valid <= kWide / 2)
+    wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, true>(p, t, row0, valid, k0, k1, smem, acc);
+  else
+    wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, false>(p, t, row0, valid, k0, k1, smem, acc);
   if (part)
     wide_store_partial(part, acc);
   else
