@@ -442,13 +442,17 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
   } while (0)
 
   for (int q = 0; q < AHEAD; ++q) EXF_W_ISSUE(q, k0 + q);
+  static_assert((BK / 16) % 2 == 0, "the last step of a stage uses fragment set 1");
+  bf16x8 fa[2][TM], fb[2][TN];
   int buf = 0;  // ring buffer of stage kt (wave-uniform)
   for (int kt = k0; kt < k1; ++kt) {
     // Wait until this wave's loads of stage kt have landed (the later stages
     // stay in flight) and its LDS reads of the previous stage are done; after
     // the barrier every wave's part of stage kt is in LDS and nobody reads the
     // previous buffer any more, so it is refilled with stage kt + AHEAD; then
-    // the k16 steps of stage kt.
+    // the k16 steps of stage kt, software-pipelined: the fragments of step s
+    // are read while the MFMAs of step s - 1 run (the last step of a stage,
+    // already in registers, runs after the next barrier).
     if (VMC == 0)
       asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     else if (VMC == 6)
@@ -463,16 +467,17 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
     EXF_W_ISSUE(prev, kt + AHEAD);
     if (!HALF || wm == 0) {
 #pragma unroll
-      for (int s2 = 0; s2 < BK / 32; ++s2) {
-        bf16x8 a0_[TM], b0_[TN], a1_[TM], b1_[TN];
-        EXF_W_FRAGS(a0_, b0_, buf, 2 * s2);
-        EXF_W_FRAGS(a1_, b1_, buf, 2 * s2 + 1);
-        EXF_W_MMA(a0_, b0_);
-        EXF_W_MMA(a1_, b1_);
+      for (int s_ = 0; s_ < BK / 16; ++s_) {
+        EXF_W_FRAGS(fa[s_ & 1], fb[s_ & 1], buf, s_);
+        if (s_ > 0)
+          EXF_W_MMA(fa[(s_ - 1) & 1], fb[(s_ - 1) & 1]);
+        else if (kt > k0)
+          EXF_W_MMA(fa[1], fb[1]);
       }
     }
     buf = (buf == STAGES - 1) ? 0 : buf + 1;
   }
+  if (!HALF || wm == 0) EXF_W_MMA(fa[1], fb[1]);
   // the clamped loads past the end land before the ring is refilled or released,
   // and no wave still reads it
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
