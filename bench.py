@@ -49,7 +49,9 @@ from paper_2608_24938_amd.measure import (PEAK_BF16_TFLOPS, PEAK_HBM_GBS, HipEve
 
 METRIC = "folded MoE layer: prefill TFLOP/s + %MFMA peak; decode µs/layer + HBM GB/s"
 COPY_BYTES = 1 << 30        # size of the calibration copy
-DOMINANT = "expert_gemm_wide<64, 2>"   # prefill gate/up GEMM with fused SiLU*up (256x256 tiles)
+# the dominant launch: the prefill gate/up GEMM with fused SiLU*up (256x256 tiles) and the fixup of its
+# split remainder (both inside the gate/up stage the events time)
+DOMINANT = ("expert_gate_up_wide", "expert_wide_fixup<true, false>")
 KERNEL_SOURCES = ["paper_2608_24938_amd/csrc/k_gemm.hip", "paper_2608_24938_amd/csrc/common.hpp",
                   "paper_2608_24938_amd/csrc/kernels.hpp", "paper_2608_24938_amd/build.py"]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "expert_gemm_gate_up_mixtral_prefill_traffic.md")
@@ -271,7 +273,7 @@ def main():
                      "traffic": None if traffic is None else traffic["bytes_per_launch"],
                      "traffic_unit": "bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)",
                      "algorithmic_bytes": gu_bytes,
-                     "kernel": DOMINANT + " (prefill gate/up GEMM, fused SiLU*up)",
+                     "kernel": " + ".join(DOMINANT) + " (prefill gate/up GEMM, fused SiLU*up)",
                      "per_launch_gflop": round(gu_flops / 1e9, 2), "avg_launch_us": round(gate_up_us, 1)},
         "cpu_baseline": cpu,
     }
@@ -375,6 +377,7 @@ def prof_summary(d, workload, steps):
                  "HBM read MB/launch | HBM write MB/launch |")
     lines.append("|---|---|---|---|---|---|---|---|")
     record = None
+    dom = {"avg_us": 0.0, "timed": 0.0, "rd": 0.0, "wt": 0.0, "grids": [], "found": 0}
     for key, v in sorted(durs.items(), key=lambda kv: -sum(kv[1])):
         name = key[0].replace("exfold::", "").replace("(GemmKArgs)", "").replace("void ", "")
         rd = mean(fe[key]["FETCH_SIZE"]) * 1024 * f_fac if key in fe else None
@@ -383,16 +386,25 @@ def prof_summary(d, workload, steps):
         timed = mean(v[-2 * steps:-steps]) if len(v) >= 2 * steps else mean(v)
         lines.append(f"| `{name[:80]}` | {key[1]} | {len(v)} | {mean(v):.1f} | {timed:.1f} | {min(v):.1f} | "
                      f"{fmt(rd)} | {fmt(wt)} |")
-        if record is None and DOMINANT in key[0] and rd is not None and wt is not None:
-            record = {"workload": workload, "kernel": DOMINANT, "grid": key[1], "avg_us": round(mean(v), 1),
-                      "avg_us_timed_steps": round(timed, 1),
-                      "fetch_bytes": round(rd), "write_bytes": round(wt), "bytes_per_launch": round(rd + wt),
-                      "fetch_scale": round(f_fac, 4), "write_scale": round(w_fac, 4),
-                      "sources_sha256": kernel_sources_sha256()}
+        part = next((i for i, n in enumerate(DOMINANT) if n in key[0]), None)
+        if part is not None and rd is not None and wt is not None and not dom["found"] & (1 << part):
+            dom["found"] |= 1 << part
+            dom["avg_us"] += mean(v)
+            dom["timed"] += timed
+            dom["rd"] += rd
+            dom["wt"] += wt
+            dom["grids"].append(key[1])
+    if dom["found"] == (1 << len(DOMINANT)) - 1:
+        record = {"workload": workload, "kernel": " + ".join(DOMINANT), "grid": dom["grids"],
+                  "avg_us": round(dom["avg_us"], 1), "avg_us_timed_steps": round(dom["timed"], 1),
+                  "fetch_bytes": round(dom["rd"]), "write_bytes": round(dom["wt"]),
+                  "bytes_per_launch": round(dom["rd"] + dom["wt"]),
+                  "fetch_scale": round(f_fac, 4), "write_scale": round(w_fac, 4),
+                  "sources_sha256": kernel_sources_sha256()}
     lines.append("")
     if record is not None:
-        lines.append("The dominant kernel is the launch of the prefill gate/up GEMM with the largest total time; "
-                     "its traffic (read + write, scaled) per launch:")
+        lines.append("The dominant launch is the prefill gate/up GEMM and the fixup of its split remainder (the "
+                     "gate/up stage); their traffic (read + write, scaled) per launch, summed:")
         lines.append("")
         lines.append("traffic-record: " + json.dumps(record))
     return "\n".join(lines)

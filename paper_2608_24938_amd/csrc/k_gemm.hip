@@ -469,10 +469,18 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
 #pragma unroll
       for (int s_ = 0; s_ < BK / 16; ++s_) {
         EXF_W_FRAGS(fa[s_ & 1], fb[s_ & 1], buf, s_);
-        if (s_ > 0)
+        if (s_ > 0) {
           EXF_W_MMA(fa[(s_ - 1) & 1], fb[(s_ - 1) & 1]);
-        else if (kt > k0)
+          // one LDS read after each of the first TM + TN MFMAs
+#pragma unroll
+          for (int g_ = 0; g_ < TM + TN; ++g_) {
+            __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+            __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+          }
+          __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - TM - TN, 0);
+        } else if (kt > k0) {
           EXF_W_MMA(fa[1], fb[1]);
+        }
       }
     }
     buf = (buf == STAGES - 1) ? 0 : buf + 1;
