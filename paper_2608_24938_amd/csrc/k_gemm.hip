@@ -57,6 +57,7 @@ __device__ __forceinline__ int swz(int r, int q) { return (r * 8 + (q ^ ((r ^ (r
 // equal, contiguous share of the real tiles.
 struct TileId {
   int g, nt, ks, mt;
+  int dbl;  // wide tiles: a 128-row tail spanning n-tiles nt and nt + 1
 };
 // Tile of logical id L (m-tile fastest within a group and n-tile).
 __device__ __forceinline__ void tile_at(const GemmKArgs &p, int L, TileId &t) {
@@ -303,10 +304,13 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
 }
 
 // ---------------------------------------------------------------------------
-// Wide tile for the prefill gate/up GEMM (many rows per retained expert):
-// 256x256 macro tile, eight waves (two per SIMD), wave (wm, wn) owning tile
-// rows 128 wm .. 128 wm + 127 and gate columns 32 wn .. 32 wn + 31 with the
-// matching up columns (4x2 MFMA tiles).  The operands go from global memory
+// Wide tile for the prefill GEMMs (many rows per retained expert): 256x256
+// macro tile, eight waves (two per SIMD), wave (wm, wn) owning tile rows
+// 128 wm .. 128 wm + 127 and 64 columns (gate/up: gate columns 32 wn .. 32 wn +
+// 31 with the matching up columns; 4x2 MFMA tiles); a group's last rows, when
+// at most 128, form a 128x512 tile over two n-tiles (the waves in one row).
+// Four waves of 128x128 each (one per SIMD, accumulators in AGPRs) measured
+// 7-11% slower.  The operands go from global memory
 // straight into LDS (global_load_lds_dwordx4) through a ring of reduction
 // stages: no staging registers and no LDS write instructions.  Against 128x128
 // tiles the bytes loaded per flop halve, and the weight panel a tile shares
@@ -332,6 +336,38 @@ __device__ __forceinline__ void lds_dma16(const void *g, uint32_t lds) {
                : "memory", "m0");
 }
 
+// Wide tile of logical id L.  The tile list counts rows of a group in
+// 128-row units (u_g = ceil(rows_g / 128), prefix tile_start); per group and
+// per pair j of n-tiles (2j, 2j + 1) there are u_g tiles: the M = u_g / 2
+// full-height m-tiles of n-tile 2j, then those of n-tile 2j + 1 (m-tile
+// fastest: the tiles that share a weight panel run side by side), then, for
+// odd u_g, one tail tile of at most 128 rows that spans both n-tiles.  The
+// tail costs half a tile and starts and ends with its neighbours, so the tiles
+// that share a panel stay in step (a half-height tile on one n-tile would run
+// ahead of its siblings and fetch the panel a second time).
+__device__ __forceinline__ void wide_tile_at(const GemmKArgs &p, int L, TileId &t) {
+  const int pairs = p.n_tiles / 2;
+  int lo = 0, hi = p.groups;
+  while (hi - lo > 1) {
+    const int mid = (lo + hi) >> 1;
+    if (p.tile_start[mid] * pairs <= L) lo = mid; else hi = mid;
+  }
+  const int u_g = p.tile_start[lo + 1] - p.tile_start[lo];
+  const int local = L - p.tile_start[lo] * pairs;
+  const int j = local / u_g, u = local % u_g, M = u_g >> 1;
+  t.g = lo;
+  t.ks = 0;
+  if (u < 2 * M) {
+    t.nt = 2 * j + u / M;
+    t.mt = u % M;
+    t.dbl = 0;
+  } else {
+    t.nt = 2 * j;
+    t.mt = M;
+    t.dbl = 1;
+  }
+}
+
 // Slot of 16-byte chunk q in a tile row of BK bf16 (an involution in q): the
 // chunk columns that one ds_read_b128 takes from consecutive rows land in
 // distinct LDS banks.  64-byte rows: q ^ bits 2..3 of r; 128-byte rows: the
@@ -342,22 +378,28 @@ __device__ __forceinline__ int wide_slot(int r, int q) {
   return q ^ ((r ^ (r >> 1)) & 7);
 }
 
-constexpr int kWideTM = 4, kWideTN = 2;  // 32x32 MFMA tiles per wave
+// 32x32 MFMA tiles per wave: the waves form two rows of kWideWaves / 2, each
+// wave owning 128 tile rows and 32 kWideTN of the 256 tile columns
+constexpr int kWideTM = 4, kWideTN = 16 / kWideWaves;
+constexpr int kWideBN = 32 * kWideTN * (kWideWaves / 2);  // tile columns (gate/up: weight rows)
+static_assert(kWideBN == kWide, "square wide tile");
+// LDS ring: two stages of the 256 x 256 tile (128 KiB) or of the 128 x 512 tail (160 KiB)
+constexpr int kWideSmemElems = kWideStages * (kWide / 2 + 2 * kWideBN) * kWideBK;
 
 // Main loop of one wide tile over the reduction stages [k0, k1): zeroes acc,
 // streams the stages through the LDS ring and leaves the products in acc.
 // All waves of the workgroup call it; it ends with every load landed and a
-// barrier, so the ring may be refilled right after.  HALF (a group's last
-// tile holding at most 128 rows): the A rows 128..255 are not loaded and the
-// waves owning them skip their MFMAs (their accumulators stay zero).
-template <bool GATE_UP, int BK, int STAGES, int NW, bool HALF>
+// barrier, so the ring may be refilled right after.  DBL: the 128 x 512 tail
+// tile (one row of NW waves) instead of 256 x 256 (two rows of NW / 2).
+template <bool GATE_UP, int BK, int STAGES, int NW, bool DBL>
 __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &t, int row0, int valid,
                                               int k0, int k1, bf16_t *smem,
                                               f32x16 (&acc)[kWideTM][kWideTN]) {
-  // NW waves in two rows of NW / 2; each wave owns 128 rows and 64 output columns
-  // (gate/up: 32 gate + 32 up columns)
-  constexpr int WN = NW / 2;
-  constexpr int BM = kWide, BN = 64 * WN, TM = kWideTM, TN = kWideTN;
+  // NW waves in WM rows of WN; each wave owns 128 rows and 32 TN columns
+  // (gate/up: 16 TN gate + the matching 16 TN up columns)
+  constexpr int WM = DBL ? 1 : 2, WN = NW / WM;
+  constexpr int BM = 128 * WM, TM = kWideTM, TN = kWideTN, BN = 32 * TN * WN;
+  static_assert(NW == kWideWaves, "accumulator shape");
   constexpr int STAGE = (BM + BN) * BK;          // elements of one stage (A rows, then B rows)
   constexpr int CPR = BK / 8;                    // 16-byte chunks per row
   constexpr int RPB = 64 / CPR;                  // rows per 1 KiB block
@@ -367,8 +409,7 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
   constexpr int VMC = (AHEAD - 1) * PW;          // loads allowed in flight at a stage's wait
   static_assert(VMC == 0 || VMC == 6 || VMC == 8 || VMC == 12 || VMC == 16, "vmcnt immediates below");
   static_assert(BLOCKS % NW == 0, "blocks per wave");
-  static_assert(!HALF || VMC == 0, "HALF issues fewer loads per stage: one stage in flight only");
-  static_assert((NW * RPB) % (BM / 2) == 0 || (BM / 2) % (NW * RPB) == 0, "A halves by load index");
+  static_assert(STAGES * STAGE <= kWideSmemElems, "LDS ring");
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -394,9 +435,9 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
       const int q = wide_slot<BK>(rb, lane % CPR);
       int wrow;
       if (GATE_UP)
-        wrow = (rb < BN / 2) ? t.nt * (BN / 2) + rb : p.inter + t.nt * (BN / 2) + (rb - BN / 2);
+        wrow = (rb < BN / 2) ? t.nt * (kWideBN / 2) + rb : p.inter + t.nt * (kWideBN / 2) + (rb - BN / 2);
       else
-        wrow = t.nt * BN + rb;
+        wrow = t.nt * kWideBN + rb;
       src[i] = Wg + (long long)wrow * p.ldw + (long long)t.ks * p.kc + q * 8;
     }
   }
@@ -412,7 +453,9 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
 #pragma unroll
   for (int i = 0; i < TM; ++i) a_row[i] = wm * 128 + i * 32 + (lane & 31);
 #pragma unroll
-  for (int j = 0; j < TN; ++j) b_row[j] = (GATE_UP ? j * (BN / 2) + wn * 32 : wn * 64 + j * 32) + (lane & 31);
+  for (int j = 0; j < TN; ++j)
+    b_row[j] = (GATE_UP ? (j < TN / 2 ? 0 : BN / 2) + (j % (TN / 2)) * 32 + wn * 16 * TN : wn * 32 * TN + j * 32) +
+               (lane & 31);
 
   // Stage kt (clamped to the last of the range: loads past it refill a buffer
   // that is never read again) into ring buffer BUF.
@@ -421,8 +464,7 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
     const int k0_ = min((KT_), k1 - 1) * BK;                                                   \
     const uint32_t base_ = lds0 + (uint32_t)(BUF) * (STAGE * 2);                               \
     _Pragma("unroll") for (int i_ = 0; i_ < PW; ++i_)                                          \
-        if (!HALF || i_ * NW * RPB < BM / 2 || i_ * NW * RPB >= BM)                            \
-            lds_dma16(src[i_] + k0_, base_ + (i_ * NW + wave) * 1024);                         \
+        lds_dma16(src[i_] + k0_, base_ + (i_ * NW + wave) * 1024);                             \
   } while (0)
 #define EXF_W_FRAGS(A_, B_, BUF, S_)                                                           \
   do {                                                                                         \
@@ -465,7 +507,7 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
       asm volatile("s_waitcnt vmcnt(16) lgkmcnt(0)\n\ts_barrier" ::: "memory");
     const int prev = (buf == 0) ? STAGES - 1 : buf - 1;
     EXF_W_ISSUE(prev, kt + AHEAD);
-    if (!HALF || wm == 0) {
+    {
 #pragma unroll
       for (int s_ = 0; s_ < BK / 16; ++s_) {
         EXF_W_FRAGS(fa[s_ & 1], fb[s_ & 1], buf, s_);
@@ -485,7 +527,7 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
     }
     buf = (buf == STAGES - 1) ? 0 : buf + 1;
   }
-  if (!HALF || wm == 0) EXF_W_MMA(fa[1], fb[1]);
+  EXF_W_MMA(fa[1], fb[1]);
   // the clamped loads past the end land before the ring is refilled or released,
   // and no wave still reads it
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
@@ -503,10 +545,10 @@ __device__ __forceinline__ int wide_row(int wm, int i, int r, int lane) {
 
 // Finished tile: gate/up writes H = SiLU(gate) * up; down scales by the row's
 // routing weight and writes y (direct), bf16 rows Yh or fp32 rows Y.
-template <bool GATE_UP, bool DIRECT, int NW>
+template <bool GATE_UP, bool DIRECT, int NW, bool DBL>
 __device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, int row0, int valid,
                                            const f32x16 (&acc)[kWideTM][kWideTN]) {
-  constexpr int WN = NW / 2, BN = 64 * WN;
+  constexpr int WN = DBL ? NW : NW / 2, TN = kWideTN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
 #pragma unroll
@@ -517,13 +559,16 @@ __device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, 
       if (ml < valid) {
         const int row = row0 + ml;
         if (GATE_UP) {
-          const int n = t.nt * (BN / 2) + wn * 32 + (lane & 31);
-          p.H[(long long)row * p.inter + n] = f32_to_bf16(silu(acc[i][0][r]) * acc[i][1][r]);
+#pragma unroll
+          for (int j = 0; j < TN / 2; ++j) {
+            const int n = t.nt * (kWideBN / 2) + wn * 16 * TN + j * 32 + (lane & 31);
+            p.H[(long long)row * p.inter + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + TN / 2][r]);
+          }
         } else {
           const float w = p.row_w[row];
 #pragma unroll
           for (int j = 0; j < kWideTN; ++j) {
-            const int n = t.nt * BN + wn * 64 + j * 32 + (lane & 31);
+            const int n = t.nt * kWideBN + wn * 32 * TN + j * 32 + (lane & 31);
             const float v = acc[i][j][r] * w;
             if (DIRECT)
               p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v);
@@ -563,23 +608,26 @@ struct WideSplit {
   int s;
 };
 __device__ __forceinline__ WideSplit wide_split(const GemmKArgs &p, int G) {
-  const int total = p.tile_start[p.groups] * p.n_tiles;
+  const int total = p.tile_start[p.groups] * (p.n_tiles / 2);
   const int rem = total % G;
   const int s = rem > 0 ? min(G / rem, min(kWideMaxSplit, p.kc / kWideBK / 4)) : 1;
   if (rem > 0 && s >= 2) return WideSplit{total - rem, rem, s};
   return WideSplit{total, 0, 1};
 }
 
+// Partial tile in the accumulator layout: row-major, 256 (DBL: 512) columns.
+template <bool DBL>
 __device__ __forceinline__ void wide_store_partial(float *P, const f32x16 (&acc)[kWideTM][kWideTN]) {
+  constexpr int WN = DBL ? kWideWaves : kWideWaves / 2, BN = 32 * kWideTN * WN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int wm = wave >> 2, wn = wave & 3;
+  const int wm = wave / WN, wn = wave % WN;
 #pragma unroll
   for (int i = 0; i < kWideTM; ++i)
 #pragma unroll
     for (int j = 0; j < kWideTN; ++j)
 #pragma unroll
       for (int r = 0; r < 16; ++r)
-        P[wide_row(wm, i, r, lane) * kWide + wn * 64 + j * 32 + (lane & 31)] = acc[i][j][r];
+        P[wide_row(wm, i, r, lane) * BN + wn * 32 * kWideTN + j * 32 + (lane & 31)] = acc[i][j][r];
 }
 
 // Workgroup blockIdx.x of a launch of ndp + rem s workgroups (more exit).
@@ -593,30 +641,35 @@ __device__ __forceinline__ void wide_gemm(const GemmKArgs &p, int G, bf16_t *sme
   int k0 = 0, k1 = KT;
   float *part = nullptr;
   if (b < w.ndp) {
-    tile_at(p, xcd_remap(b, w.ndp), t);
+    wide_tile_at(p, xcd_remap(b, w.ndp), t);
   } else {
     const int j = b - w.ndp, n = w.rem * w.s;
     if (j >= n) return;
     const int lj = xcd_remap(j, n), c = lj / w.rem, r = lj % w.rem;
-    tile_at(p, w.ndp + r, t);
+    wide_tile_at(p, w.ndp + r, t);
     k0 = c * KT / w.s;
     k1 = (c + 1) * KT / w.s;
     part = p.P + (size_t)(r * w.s + c) * kWideTileElems;
   }
   const int row0 = p.offsets[t.g] + t.mt * kWide;
-  const int valid = min(kWide, p.offsets[t.g + 1] - row0);
   f32x16 acc[kWideTM][kWideTN];
-  if (valid <= kWide / 2)
+  if (__builtin_amdgcn_readfirstlane(t.dbl)) {
+    const int valid = min(kWide / 2, p.offsets[t.g + 1] - row0);
     wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, true>(p, t, row0, valid, k0, k1, smem, acc);
-  else
+    if (part)
+      wide_store_partial<true>(part, acc);
+    else
+      wide_store<GATE_UP, DIRECT, NW, true>(p, t, row0, valid, acc);
+  } else {
+    const int valid = min(kWide, p.offsets[t.g + 1] - row0);
     wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, false>(p, t, row0, valid, k0, k1, smem, acc);
-  if (part)
-    wide_store_partial(part, acc);
-  else
-    wide_store<GATE_UP, DIRECT, NW>(p, t, row0, valid, acc);
+    if (part)
+      wide_store_partial<false>(part, acc);
+    else
+      wide_store<GATE_UP, DIRECT, NW, false>(p, t, row0, valid, acc);
+  }
 }
 
-constexpr int kWideSmemElems = kWideStages * (kWide + 32 * kWideWaves) * kWideBK;
 
 __global__ __launch_bounds__(64 * kWideWaves, 1) void expert_gate_up_wide(const GemmKArgs p, int G) {
   __shared__ __attribute__((aligned(1024))) bf16_t smem[kWideSmemElems];
@@ -630,22 +683,23 @@ __global__ __launch_bounds__(64 * kWideWaves, 1) void expert_down_wide(const Gem
 }
 
 // Block (r, c): remainder tile r, tile rows 16 c .. 16 c + 15, sixteen threads
-// a row.  Gate/up: H columns 128 nt + col from the gate partials (column
-// 64 (col / 32) + col % 32) and the up partials 32 columns further; down: the
-// 256 output columns scaled by the row's routing weight.
+// a row.  Gate/up: H columns 128 nt + col from the gate and up partials laid
+// out as the accumulators of the waves (wide_store_partial); down: the 256
+// (tail tile: 512) output columns scaled by the row's routing weight.
 template <bool GATE_UP, bool DIRECT>
 __global__ __launch_bounds__(256) void expert_wide_fixup(const GemmKArgs p, int G) {
   const WideSplit w = wide_split(p, G);
   const int r = blockIdx.x;
   if (r >= w.rem) return;
   TileId t;
-  tile_at(p, w.ndp + r, t);
+  wide_tile_at(p, w.ndp + r, t);
+  const int bm = t.dbl ? kWide / 2 : kWide, bn = t.dbl ? 2 * kWideBN : kWideBN;
   const int row0 = p.offsets[t.g] + t.mt * kWide;
-  const int valid = min(kWide, p.offsets[t.g + 1] - row0);
+  const int valid = min(bm, p.offsets[t.g + 1] - row0);
   const int ml = blockIdx.y * 16 + (threadIdx.x >> 4);
   if (ml >= valid) return;
   const int row = row0 + ml;
-  const float *P0 = p.P + (size_t)r * w.s * kWideTileElems + (size_t)ml * kWide;
+  const float *P0 = p.P + (size_t)r * w.s * kWideTileElems + (size_t)ml * bn;
   auto sum4 = [&](int col) {
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
     for (int k = 0; k < w.s; ++k) {
@@ -658,26 +712,25 @@ __global__ __launch_bounds__(256) void expert_wide_fixup(const GemmKArgs p, int 
     return v;
   };
   if (GATE_UP) {
-#pragma unroll
-    for (int q = 0; q < 2; ++q) {
+    for (int q = 0; q < bn / 128; ++q) {
       const int col = q * 64 + (threadIdx.x & 15) * 4;
-      const int pc = (col >> 5) * 64 + (col & 31);
-      const float4 g = sum4(pc), u = sum4(pc + 32);
+      // gate tile (col / 32) % (TN / 2) of wave col / (16 TN); its up tile TN / 2 further
+      const int pc = (col / (16 * kWideTN)) * 32 * kWideTN + ((col >> 5) % (kWideTN / 2)) * 32 + (col & 31);
+      const float4 g = sum4(pc), u = sum4(pc + 16 * kWideTN);
       const float h[4] = {silu(g.x) * u.x, silu(g.y) * u.y, silu(g.z) * u.z, silu(g.w) * u.w};
-      bf16_t *dst = p.H + (long long)row * p.inter + t.nt * (kWide / 2) + col;
+      bf16_t *dst = p.H + (long long)row * p.inter + t.nt * (kWideBN / 2) + col;
 #pragma unroll
       for (int e = 0; e < 4; ++e) dst[e] = f32_to_bf16(h[e]);
     }
   } else {
     const float rw = p.row_w[row];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
+    for (int q = 0; q < bn / 64; ++q) {
       const int col = q * 64 + (threadIdx.x & 15) * 4;
       const float4 a = sum4(col);
       const float v[4] = {a.x * rw, a.y * rw, a.z * rw, a.w * rw};
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
-        const int n = t.nt * kWide + col + e;
+        const int n = t.nt * kWideBN + col + e;
         if (DIRECT)
           p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v[e]);
         else if (p.Yh)
@@ -942,24 +995,25 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
   // tiles on average): 256x256 gate/up tiles.  Below that the partial tiles of
   // a skewed load cost more than the wide tile saves (Qwen3-shaped prefill,
   // 256 rows per expert: even).
-  const bool gu_wide = !gu_skinny && inter % 128 == 0 && d % 128 == 0 && 2 * rows >= 3 * kWide * active;
+  const bool gu_wide = !gu_skinny && inter % kWideBN == 0 && d % 128 == 0 && 2 * rows >= 3 * kWide * active;
   const bool dn_skinny = sk_shapes && rows <= 64 * active;
   if (gu_skinny) {
     *gu = GemmPlan{kSkM, kSkN, 1, 0, kGemmSkinny};
     gu->grid = (rows / kSkM + groups) * (inter / (kSkN / 2));  // >= sum of ceil(rows_g / 32) tiles
   } else if (gu_wide) {
-    // whole rounds plus the split remainder: at most ceil tiles + one round
-    *gu = GemmPlan{kWide, 64 * (kWideWaves / 2), 1, 0, kGemmWide, cu_count};
-    gu->grid = (rows / kWide + groups) * (inter / (32 * (kWideWaves / 2))) + cu_count;
+    // tile list in 128-row units, one tile per unit and pair of 128-column
+    // n-tiles; whole rounds plus the split remainder: at most that + one round
+    *gu = GemmPlan{kWide / 2, kWideBN, 1, 0, kGemmWide, cu_count};
+    gu->grid = (rows / 128 + groups) * (inter / kWideBN) + cu_count;
   } else {
     *gu = GemmPlan{128, 128, 1, 0, kGemmTile};
     gu->grid = (rows / 128 + groups) * (inter / 64);
   }
   // Down projection on the wide tile where the gate/up projection takes it and
   // the tiles (at least rows / 256 per 256 output columns) fill one round.
-  if (!dn_skinny && gu_wide && d % kWide == 0 && (long long)(rows / kWide) * (d / kWide) >= cu_count) {
-    *dn = GemmPlan{kWide, kWide, 1, 0, kGemmWide, cu_count};
-    dn->grid = (rows / kWide + groups) * (d / kWide) + cu_count;
+  if (!dn_skinny && gu_wide && d % (2 * kWideBN) == 0 && (long long)(rows / kWide) * (d / kWide) >= cu_count) {
+    *dn = GemmPlan{kWide / 2, kWideBN, 1, 0, kGemmWide, cu_count};
+    dn->grid = (rows / 128 + groups) * (d / (2 * kWideBN)) + cu_count;
     return;
   }
   // Few expected tiles: split the down projection's reduction so the workgroups

@@ -71,7 +71,8 @@ hipError_t launch_static_pool(const float *h, int N, int D, const float *S, cons
 // `wgs` workgroups, a short last round split along the reduction.
 enum { kGemmSimt = 0, kGemmTile = 1, kGemmSkinny = 2, kGemmWide = 3 };
 struct GemmPlan {
-  int bm, bn;  // tile height (rows) and width (output columns, or weight rows for gate/up)
+  int bm, bn;  // tile height (rows; kGemmWide: the 128-row unit of its tile list) and width
+               // (output columns, or weight rows for gate/up)
   int ksplit;  // splits of the reduction (down projection only; partial outputs)
   int grid;    // workgroups launched (an upper bound on the device-side tile count)
   int kind;    // kGemmSimt (float32 layers), kGemmTile, kGemmSkinny or kGemmWide (bf16 MFMA tiles)

@@ -250,10 +250,13 @@ def test_execute_every_kernel_path(shape_name, T, k_out):
     assert err.max() <= TOL_Y["bf16"], err.max()
 
 
-# Wide 256x256 tiles for both GEMMs (2 rows >= 3 x 256 per expert and at
-# least one round of down tiles): whole rounds of one tile per CU, then a short
-# last round whose tiles are split along the reduction and finished by the
-# fixup kernel.
+# Wide tiles for both GEMMs (2 rows >= 3 x 256 per expert and at least one
+# round of down tiles): whole rounds of one tile per CU, then a short last
+# round whose tiles are split along the reduction and finished by the fixup
+# kernel.  The wide tile list counts rows in 128-row units u_g = ceil(rows_g /
+# 128) per pair of n-tiles (gate/up: inter / 256 pairs, down: d / 512); a
+# group whose last tile holds at most 128 rows ends in one 128 x 512 tail tile
+# per pair.
 SPLIT_SHAPE = synth.LayerShape("wide-split", d=2048, inter=1024, n_experts=8, top_k=2, dtype="bf16")
 
 
@@ -265,38 +268,45 @@ def _routes_with_counts(counts, k_out, rng):
     return ids[rng.permutation(T)]
 
 
-def _wide_split(tiles, G):
+def _wide_split(tiles, G, KT):
     """(whole tiles, remainder tiles, split) of a wide launch of `tiles` tiles in rounds of G."""
     rem = tiles % G
-    return (tiles - rem, rem, G // rem) if rem and 2 * rem <= G else (tiles, 0, 1)
+    s = min(G // rem, 16, KT // 4) if rem else 1
+    return (tiles - rem, rem, s) if rem and s >= 2 else (tiles, 0, 1)
 
 
-# counts -> m-tiles of 256 rows: 38 (both GEMMs 304 tiles: 48 split 5 / 4 ways),
-# 48 (384 tiles: 128 split twice, the largest split remainder) and 50 (400
-# tiles: 144 left whole)
-SPLIT_COUNTS = {38: [1300, 1200, 1100, 1000, 1400, 1000, 1000, 1000],
-                48: [1500, 1500, 1536, 1537, 1200, 1300, 1400, 1300],
-                50: [1500, 1500, 1536, 1538, 1290, 1300, 1400, 1540]}
+# units (sum of ceil(rows / 128)) -> route counts; 4 units per pair of n-tiles
+# for both GEMMs: 75 units = 300 tiles (44 split 5 ways for gate/up, 4 for
+# down; tails of each kind), 96 = 384 (128 split twice, the largest split
+# remainder), 100 = 400 (144 left whole)
+SPLIT_COUNTS = {75: [1300, 1200, 1100, 1000, 1400, 1024, 1100, 1100],
+                96: [1500, 1500, 1537, 1538, 1290, 1300, 1400, 1540],
+                100: [1500, 1500, 1537, 1538, 1290, 1300, 1400, 2101]}
 
 
-@pytest.mark.parametrize("mtiles,k_out", [(38, 1), (38, 2), (48, 1), (50, 2)])
-def test_execute_wide_split_remainder(mtiles, k_out):
+@pytest.mark.parametrize("units,k_out", [(75, 1), (75, 2), (96, 1), (100, 2)])
+def test_execute_wide_split_remainder(units, k_out):
     shape = SPLIT_SHAPE
-    counts = np.array(SPLIT_COUNTS[mtiles])
-    assert int(np.ceil(counts / 256).sum()) == mtiles
+    counts = np.array(SPLIT_COUNTS[units])
+    assert int(np.ceil(counts / 128).sum()) == units
     G = torch.cuda.get_device_properties(0).multi_processor_count
-    tiles = mtiles * (shape.d // 256)          # = mtiles * (inter // 128) for the gate/up GEMM
-    print(f"wide split: {mtiles} m-tiles, k_out={k_out}, G={G}: whole/rem/split {_wide_split(tiles, G)}",
-          flush=True)
+    tiles = units * (shape.inter // 256)          # = units * (d // 512) for the down GEMM
+    print(f"wide split: {units} units, k_out={k_out}, G={G}: whole/rem/split gate/up "
+          f"{_wide_split(tiles, G, shape.d // 64)}, down {_wide_split(tiles, G, shape.inter // 64)}", flush=True)
     lp = LayerPair(shape, seed=17)
-    rng = np.random.default_rng(mtiles * 10 + k_out)
+    rng = np.random.default_rng(units * 10 + k_out)
     ids = _routes_with_counts(counts, k_out, rng)
     T = ids.shape[0]
     w = rng.standard_normal((T, k_out)).astype(np.float32)
     xs = synth.tokens(shape, T, seed=17)
     y = from_dev(X.moe_execute(lp.dev, to_dev(xs), to_dev(ids), to_dev(w)))
     sync()
-    smp = np.sort(np.concatenate([[0, T - 1], rng.choice(np.arange(1, T - 1), 254, replace=False)]))
+    # sampled tokens: the ends, a random spread, and every token routed to the
+    # last rows of each expert (the tail tiles)
+    order = np.argsort(ids[:, 0], kind="stable")
+    ends = np.cumsum(np.bincount(ids[:, 0], minlength=shape.n_experts))
+    tails = np.concatenate([order[max(0, e - 8):e] for e in ends])
+    smp = np.unique(np.concatenate([[0, T - 1], rng.choice(np.arange(1, T - 1), 254, replace=False), tails]))
     ref = O.moe_output(lp.ref, synth.widen(xs[smp]), ids[smp], w[smp])
     err = per_token_rel_l2(y[smp], ref)
     assert err.max() <= TOL_Y["bf16"], err.max()
