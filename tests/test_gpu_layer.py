@@ -225,13 +225,14 @@ def test_zero_tokens_is_a_noop():
 PATH_SHAPES = {
     "bf16-256x512": synth.LayerShape("paths", d=256, inter=512, n_experts=8, top_k=2, dtype="bf16"),
     "bf16-384x192": synth.LayerShape("paths-odd", d=384, inter=192, n_experts=8, top_k=2, dtype="bf16"),
-    # six 64-wide reduction stages and two 128-column gate/up slices on the wide gate/up tile
+    # at 8192 tokens: the wide gate/up tile with six 64-wide reduction stages and one pair of
+    # 128-column gate/up slices (below that the skinny tile)
     "bf16-384x256": synth.LayerShape("paths-384", d=384, inter=256, n_experts=8, top_k=2, dtype="bf16"),
 }
 
 
 @pytest.mark.parametrize("shape_name", sorted(PATH_SHAPES))
-@pytest.mark.parametrize("T,k_out", [(48, 1), (150, 1), (400, 1), (1900, 1), (4096, 1), (2100, 2)])
+@pytest.mark.parametrize("T,k_out", [(48, 1), (150, 1), (400, 1), (1900, 1), (4096, 1), (2100, 2), (8192, 1)])
 def test_execute_every_kernel_path(shape_name, T, k_out):
     shape = PATH_SHAPES[shape_name]
     lp = LayerPair(shape, seed=11)
