@@ -318,3 +318,26 @@ def test_execute_wide_split_remainder(units, k_out):
     y2 = from_dev(X.moe_execute(lp.dev, to_dev(xs), to_dev(ids), to_dev(w)))
     sync()
     np.testing.assert_array_equal(y, y2)
+
+
+# A shared expert on the wide tiles: its rows form the last group (weights from
+# the shared tensors), with a 128-row tail tile at 4096 + 96 tokens.
+SHARED_WIDE = synth.LayerShape("shared-wide", d=2048, inter=512, n_experts=8, top_k=2, shared_inter=512,
+                               dtype="bf16")
+
+
+@pytest.mark.parametrize("T,k_out", [(4096, 2), (4192, 1)])
+def test_execute_wide_with_shared_expert(T, k_out):
+    shape = SHARED_WIDE
+    lp = LayerPair(shape, seed=19)
+    rng = np.random.default_rng(T)
+    ids = np.stack([rng.permutation(shape.n_experts)[:k_out] for _ in range(T)]).astype(np.int32)
+    w = rng.standard_normal((T, k_out)).astype(np.float32)
+    xs = synth.tokens(shape, T, seed=19)
+    y = from_dev(X.moe_execute(lp.dev, to_dev(xs), to_dev(ids), to_dev(w)))
+    sync()
+    smp = np.unique(np.concatenate([[0, T - 1], np.arange(T - 100, T), rng.choice(T, 200, replace=False)]))
+    ref = O.moe_output(lp.ref, synth.widen(xs[smp]), ids[smp], w[smp])
+    err = per_token_rel_l2(y[smp], ref)
+    assert err.max() <= TOL_Y["bf16"], err.max()
+    assert np.isfinite(y).all()
