@@ -13,7 +13,8 @@ Mixtral-, Qwen3- and GLM-shaped prefill and decode cases) on one GPU:
 * the same forward captured once in a HIP graph and replayed (warm), which
   removes the host's launch overhead between the layer's kernels;
 * median, p10 and p90 over the repetitions; the spread of the median over eight
-  further token batches (the pool and the routes change with the tokens);
+  further token batches (the pool and the routes change with the tokens; each
+  batch gets two untimed forwards first);
 * the stage breakdown of one instrumented forward, and the folding overhead:
   router + Top-K/selection/fold + permutation as a share of the layer;
 * experts touched and rows per expert (max / mean over touched experts);
@@ -126,6 +127,8 @@ def run_config(name, wl, layer, dev, args, ev, stream, scratch):
     batch_medians = []
     for i in range(N_BATCHES):
         xi = dev(synth.tokens(shape, T, seed=100 + i))
+        for _ in range(2):      # untimed: the first forwards on a new batch pay one-time costs
+            folded(xi)
         batch_medians.append(float(np.median(_time(X, ev, stream, lambda: folded(xi), max(5, reps // 4),
                                                    scratch))))
     st = _stages(X, ev, stream, lambda a: folded(events=a))
