@@ -18,6 +18,9 @@
  *            row-major, unless stated otherwise.  Outputs and workspaces are
  *            allocated by the caller; the library allocates no device memory
  *            and keeps no state besides a read-only cache of device properties.
+ *            The layer's weights and the token tensors x, y and x_cal are read
+ *            and written in 16-byte vectors: their base pointers must be
+ *            16-byte aligned (else EXFOLD_ERR_ALIGN).
  * Streams.   `stream` is a hipStream_t passed as void* (NULL: the null stream).
  *            Every call only enqueues work and returns: no host synchronisation
  *            and no device-to-host copy.
@@ -59,7 +62,8 @@ enum {
   EXFOLD_ERR_WORKSPACE = 5,    /* workspace smaller than required or misaligned   */
   EXFOLD_ERR_DEVICE = 6,       /* a HIP launch or query failed                    */
   EXFOLD_ERR_UNSUPPORTED = 7,  /* valid request outside the kernels' limits       */
-  EXFOLD_ERR_ARG = 8           /* unknown phase or mode, or invalid scalar arg    */
+  EXFOLD_ERR_ARG = 8,          /* unknown phase or mode, or invalid scalar arg    */
+  EXFOLD_ERR_ALIGN = 9         /* a tensor pointer is not 16-byte aligned         */
 };
 
 enum { EXFOLD_F32 = 0, EXFOLD_BF16 = 1 };

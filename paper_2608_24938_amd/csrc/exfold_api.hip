@@ -44,10 +44,17 @@ int cu_count() {
   return cache[dev];
 }
 
+// The kernels move tensors in 16-byte vectors (loads of x and the weights,
+// stores of y).
+inline bool misaligned(const void *ptr) { return reinterpret_cast<uintptr_t>(ptr) % 16 != 0; }
+
 exfold_status check_layer(const exfold_layer *L) {
   if (!L) return EXFOLD_ERR_NULL;
   if (L->dtype != EXFOLD_F32 && L->dtype != EXFOLD_BF16) return EXFOLD_ERR_DTYPE;
   if (!L->w_router || !L->w_gate_up || !L->w_down) return EXFOLD_ERR_NULL;
+  if (misaligned(L->w_router) || misaligned(L->w_gate_up) || misaligned(L->w_down) ||
+      misaligned(L->ws_gate_up) || misaligned(L->ws_down))
+    return EXFOLD_ERR_ALIGN;
   if (L->d <= 0 || L->inter <= 0 || L->n_experts <= 0 || L->top_k <= 0 || L->shared_inter < 0)
     return EXFOLD_ERR_SHAPE;
   if (L->top_k > L->n_experts) return EXFOLD_ERR_SHAPE;
@@ -310,6 +317,7 @@ const char *exfold_status_str(exfold_status s) {
   switch (s) {
     case EXFOLD_OK: return "ok";
     case EXFOLD_ERR_NULL: return "required pointer is NULL";
+    case EXFOLD_ERR_ALIGN: return "tensor pointer not 16-byte aligned";
     case EXFOLD_ERR_SHAPE: return "size out of range or inconsistent";
     case EXFOLD_ERR_BUDGET: return "budget must be >= 1";
     case EXFOLD_ERR_DTYPE: return "unknown dtype";
@@ -436,6 +444,7 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
     return EXFOLD_ERR_ARG;
   if (T == 0) return EXFOLD_OK;
   if (!x || !y) return EXFOLD_ERR_NULL;
+  if (misaligned(x) || misaligned(y)) return EXFOLD_ERR_ALIGN;
   st = check_ws(ws, ws_bytes, p.total);
   if (st != EXFOLD_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -531,6 +540,7 @@ exfold_status exfold_moe_execute(const exfold_layer *layer, const void *x, int64
   if (st != EXFOLD_OK) return st;
   if (T == 0) return EXFOLD_OK;
   if (!x || !y || !route_ids || !route_w) return EXFOLD_ERR_NULL;
+  if (misaligned(x) || misaligned(y)) return EXFOLD_ERR_ALIGN;
   st = check_ws(ws, ws_bytes, total);
   if (st != EXFOLD_OK) return st;
   return run_exec(layer, p, x, route_ids, route_w, y, ws, debug ? debug->offsets : nullptr,
@@ -553,6 +563,7 @@ exfold_status exfold_calibrate_projectors(const exfold_layer *layer, const void 
   if (!(lambda >= 0.0) || !(clip >= 0.0)) return EXFOLD_ERR_ARG;
   if (!S || !L || !h) return EXFOLD_ERR_NULL;
   if (m > 0 && !x_cal) return EXFOLD_ERR_NULL;
+  if (misaligned(x_cal)) return EXFOLD_ERR_ALIGN;
   st = check_ws(ws, ws_bytes, p.total);
   if (st != EXFOLD_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
@@ -594,6 +605,7 @@ exfold_status exfold_calibrate_diagonal(const exfold_layer *layer, const void *x
   if (!(lambda >= 0.0)) return EXFOLD_ERR_ARG;
   if (!Dg || !Ld) return EXFOLD_ERR_NULL;
   if (m > 0 && !x_cal) return EXFOLD_ERR_NULL;
+  if (misaligned(x_cal)) return EXFOLD_ERR_ALIGN;
   st = check_ws(ws, ws_bytes, p.total);
   if (st != EXFOLD_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);

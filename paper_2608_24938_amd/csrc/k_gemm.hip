@@ -480,7 +480,7 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
   do {                                                                                         \
     _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_)                                          \
         _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) acc[i_][j_] =                        \
-            __builtin_amdgcn_mfma_f32_32x32x16_bf16(A_[i_], B_[j_], acc[i_][j_], 0, 0, 0);     \
+            __builtin_amdgcn_mfma_f32_32x32x16_bf16(B_[j_], A_[i_], acc[i_][j_], 0, 0, 0);     \
   } while (0)
 
   for (int q = 0; q < AHEAD; ++q) EXF_W_ISSUE(q, k0 + q);
@@ -538,11 +538,16 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
 #undef EXF_W_MMA
 }
 
-// Row / column of accumulator register r of MFMA tile (i, j) of wave (wm, wn):
-// tile row 128 wm + 32 i + 8 (r / 4) + 4 (lane / 32) + r % 4; the down column
-// (within the tile) 64 wn + 32 j + lane % 32.
-__device__ __forceinline__ int wide_row(int wm, int i, int r, int lane) {
-  return wm * 128 + i * 32 + (r >> 2) * 8 + (lane >> 5) * 4 + (r & 3);
+// Accumulator layout: the MFMAs take the weight fragment as their first
+// operand, so register r of tile (i, j) of wave (wm, wn) holds tile row (token)
+// 128 wm + 32 i + lane % 32 and tile column 32 TN wn + 32 j + 8 (r / 4) +
+// 4 (lane / 32) + r % 4: each lane owns four runs of four consecutive columns of
+// one row, stored 8 (bf16) or 16 (fp32) bytes at a time.
+__device__ __forceinline__ void store4_bf16(bf16_t *dst, float a, float b, float c, float d) {
+  uint2 v;
+  v.x = (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
+  v.y = (uint32_t)f32_to_bf16(c) | ((uint32_t)f32_to_bf16(d) << 16);
+  *reinterpret_cast<uint2 *>(dst) = v;
 }
 
 // Finished tile: gate/up writes H = SiLU(gate) * up; down scales by the row's
@@ -553,34 +558,41 @@ __device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, 
   constexpr int WN = DBL ? NW : NW / 2, TN = kWideTN;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
+  const int c4 = 4 * (lane >> 5);
 #pragma unroll
   for (int i = 0; i < kWideTM; ++i) {
+    const int ml = wm * 128 + i * 32 + (lane & 31);
+    if (ml >= valid) continue;
+    const int row = row0 + ml;
+    if (GATE_UP) {
+      bf16_t *dst = p.H + (long long)row * p.inter + t.nt * (kWideBN / 2) + wn * 16 * TN + c4;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int ml = wide_row(wm, i, r, lane);
-      if (ml < valid) {
-        const int row = row0 + ml;
-        if (GATE_UP) {
+      for (int j = 0; j < TN / 2; ++j)
 #pragma unroll
-          for (int j = 0; j < TN / 2; ++j) {
-            const int n = t.nt * (kWideBN / 2) + wn * 16 * TN + j * 32 + (lane & 31);
-            p.H[(long long)row * p.inter + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + TN / 2][r]);
-          }
-        } else {
-          const float w = p.row_w[row];
-#pragma unroll
-          for (int j = 0; j < kWideTN; ++j) {
-            const int n = t.nt * kWideBN + wn * 32 * TN + j * 32 + (lane & 31);
-            const float v = acc[i][j][r] * w;
-            if (DIRECT)
-              p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v);
-            else if (p.Yh)
-              p.Yh[(long long)row * p.d + n] = f32_to_bf16(v);
-            else
-              p.Y[((long long)t.ks * p.rows + row) * p.d + n] = v;
-          }
+        for (int g = 0; g < 4; ++g) {
+          const f32x16 &gt = acc[i][j], &up = acc[i][j + TN / 2];
+          store4_bf16(dst + j * 32 + 8 * g, silu(gt[4 * g]) * up[4 * g], silu(gt[4 * g + 1]) * up[4 * g + 1],
+                      silu(gt[4 * g + 2]) * up[4 * g + 2], silu(gt[4 * g + 3]) * up[4 * g + 3]);
         }
-      }
+    } else {
+      const float w = p.row_w[row];
+      const int n0 = t.nt * kWideBN + wn * 32 * TN + c4;
+      const long long base = DIRECT ? (long long)p.row_token[row] * p.d : (long long)row * p.d;
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x16 &c = acc[i][j];
+          const int n = n0 + j * 32 + 8 * g;
+          const float v0 = c[4 * g] * w, v1 = c[4 * g + 1] * w, v2 = c[4 * g + 2] * w, v3 = c[4 * g + 3] * w;
+          if (DIRECT)
+            store4_bf16(p.y + base + n, v0, v1, v2, v3);
+          else if (p.Yh)
+            store4_bf16(p.Yh + base + n, v0, v1, v2, v3);
+          else
+            *reinterpret_cast<float4 *>(p.Y + ((long long)t.ks * p.rows + row) * p.d + n) =
+                make_float4(v0, v1, v2, v3);
+        }
     }
   }
 }
@@ -624,12 +636,17 @@ __device__ __forceinline__ void wide_store_partial(float *P, const f32x16 (&acc)
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int wm = wave / WN, wn = wave % WN;
 #pragma unroll
-  for (int i = 0; i < kWideTM; ++i)
+  for (int i = 0; i < kWideTM; ++i) {
+    float *prow = P + (wm * 128 + i * 32 + (lane & 31)) * BN + wn * 32 * kWideTN + 4 * (lane >> 5);
 #pragma unroll
     for (int j = 0; j < kWideTN; ++j)
 #pragma unroll
-      for (int r = 0; r < 16; ++r)
-        P[wide_row(wm, i, r, lane) * BN + wn * 32 * kWideTN + j * 32 + (lane & 31)] = acc[i][j][r];
+      for (int g = 0; g < 4; ++g) {
+        const f32x16 &c = acc[i][j];
+        *reinterpret_cast<float4 *>(prow + j * 32 + 8 * g) =
+            make_float4(c[4 * g], c[4 * g + 1], c[4 * g + 2], c[4 * g + 3]);
+      }
+  }
 }
 
 // Workgroup blockIdx.x of a launch of ndp + rem s workgroups (more exit).

@@ -17,7 +17,7 @@ import torch
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libexfold.so")
 _lib = None
 
-OK, ERR_NULL, ERR_SHAPE, ERR_BUDGET, ERR_DTYPE, ERR_WORKSPACE, ERR_DEVICE, ERR_UNSUPPORTED, ERR_ARG = range(9)
+OK, ERR_NULL, ERR_SHAPE, ERR_BUDGET, ERR_DTYPE, ERR_WORKSPACE, ERR_DEVICE, ERR_UNSUPPORTED, ERR_ARG, ERR_ALIGN = range(10)
 F32, BF16 = 0, 1
 PHASE = {"dense": 0, "prefill": 1, "decode": 2, "decode_static": 3, "prefill_diag": 4}
 CAL_MODE = {"corouted": 0, "common": 1}

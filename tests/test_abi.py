@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in range(9):
+    for code in range(10):
         assert X.status_str(code)
     assert X.status_str(0) == "ok"
 
@@ -73,6 +73,9 @@ def forward(ly, T=64, phase=1, budget=1, tables=True, ws_bytes=None, x=FAKE, y=F
     (dict(inter=100), X.ERR_UNSUPPORTED),
     (dict(shared_inter=512), X.ERR_NULL),
     (dict(shared_inter=256, ws_gate_up=FAKE, ws_down=FAKE), X.ERR_UNSUPPORTED),
+    (dict(w_gate_up=FAKE + 8), X.ERR_ALIGN),
+    (dict(w_router=FAKE + 2), X.ERR_ALIGN),
+    (dict(shared_inter=512, ws_gate_up=FAKE, ws_down=FAKE + 4), X.ERR_ALIGN),
 ])
 def test_layer_validation(kw, code):
     ly = layer(**kw)
@@ -88,6 +91,8 @@ def test_forward_validation_codes():
     assert forward(ly, T=-1) == X.ERR_SHAPE
     assert forward(ly, tables=False) == X.ERR_NULL
     assert forward(ly, x=None) == X.ERR_NULL
+    assert forward(ly, x=FAKE + 8) == X.ERR_ALIGN        # 16-byte vectors move x and y
+    assert forward(ly, y=FAKE + 2) == X.ERR_ALIGN
     need = ws_size(ly)
     assert need > 0
     assert forward(ly, ws_bytes=need - 1) == X.ERR_WORKSPACE
@@ -178,4 +183,5 @@ def test_execute_validation():
     n = L.exfold_execute_workspace_size(ctypes.byref(ly), 64, 2)
     assert n > 0
     assert L.exfold_moe_execute(ctypes.byref(ly), f, 64, 2, None, f, f, None, f * 16, n, None) == X.ERR_NULL
+    assert L.exfold_moe_execute(ctypes.byref(ly), f + 8, 64, 2, f, f, f, None, f * 16, n, None) == X.ERR_ALIGN
     assert L.exfold_moe_execute(ctypes.byref(ly), f, 64, 2, f, f, f, None, f * 16, n - 1, None) == X.ERR_WORKSPACE

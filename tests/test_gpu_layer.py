@@ -173,10 +173,16 @@ def test_exact_multiples_fold_reproduces_full_output(dtype):
         assert err.max() <= TOL_Y[dtype], err.max()
 
 
+# 4096 calibration tokens x 2 routes: both GEMMs on the wide tiles, the per-row
+# outputs kept in float32 for the statistics
+CAL_WIDE = synth.LayerShape("cal-wide", d=2048, inter=512, n_experts=8, top_k=2, dtype="bf16")
+
+
 @pytest.mark.parametrize("shape,m,mode,lam,clip", [(synth.TINY, 512, "corouted", 1e-3, 4.0),
                                                    (synth.TINY, 200, "common", 1e-3, 0.0),
                                                    (WIDE_F32, 300, "corouted", 1e-2, 4.0),
-                                                   (SMALL_BF16, 512, "corouted", 1e-3, 4.0)])
+                                                   (SMALL_BF16, 512, "corouted", 1e-3, 4.0),
+                                                   (CAL_WIDE, 4096, "corouted", 1e-3, 4.0)])
 def test_calibration_matches_oracle(shape, m, mode, lam, clip):
     lp = LayerPair(shape, seed=7)
     xs = synth.calibration_tokens(shape, m, seed=7)
