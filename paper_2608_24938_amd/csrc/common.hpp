@@ -24,13 +24,9 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ float bf16_to_f32(bf16_t b) { return __uint_as_float(uint32_t(b) << 16); }
 
-// Round-to-nearest-even float32 -> bf16 (NaN kept quiet).
-__device__ __forceinline__ bf16_t f32_to_bf16(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return bf16_t((u >> 16) | 0x40u);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return bf16_t(u >> 16);
-}
+// Round-to-nearest-even float32 -> bf16 (the hardware conversion,
+// v_cvt_pk_bf16_f32 on gfx950).
+__device__ __forceinline__ bf16_t f32_to_bf16(float f) { return __builtin_bit_cast(bf16_t, (__bf16)f); }
 
 template <typename T> __device__ __forceinline__ float load_f32(const T *p);
 template <> __device__ __forceinline__ float load_f32<float>(const float *p) { return *p; }

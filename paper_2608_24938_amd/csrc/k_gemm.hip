@@ -41,7 +41,10 @@ struct GemmKArgs {
   const float *row_w;
 };
 
-__device__ __forceinline__ float silu(float g) { return g / (1.0f + __expf(-g)); }
+// g * sigmoid(g) with the hardware reciprocal (one rounding step instead of
+// the IEEE division sequence; the result is rounded to bf16 or kept fp32
+// within 1 ulp).
+__device__ __forceinline__ float silu(float g) { return g * __builtin_amdgcn_rcpf(1.0f + __expf(-g)); }
 
 constexpr int kBK = 64;
 
@@ -544,10 +547,9 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
 // 4 (lane / 32) + r % 4: each lane owns four runs of four consecutive columns of
 // one row, stored 8 (bf16) or 16 (fp32) bytes at a time.
 __device__ __forceinline__ void store4_bf16(bf16_t *dst, float a, float b, float c, float d) {
-  uint2 v;
-  v.x = (uint32_t)f32_to_bf16(a) | ((uint32_t)f32_to_bf16(b) << 16);
-  v.y = (uint32_t)f32_to_bf16(c) | ((uint32_t)f32_to_bf16(d) << 16);
-  *reinterpret_cast<uint2 *>(dst) = v;
+  typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+  const bf16x4 v = {(__bf16)a, (__bf16)b, (__bf16)c, (__bf16)d};   // two v_cvt_pk_bf16_f32
+  *reinterpret_cast<bf16x4 *>(dst) = v;
 }
 
 // Finished tile: gate/up writes H = SiLU(gate) * up; down scales by the row's
