@@ -12,6 +12,7 @@
 namespace exfold {
 
 constexpr int kPermThreads = 256;
+constexpr int kScanLdsInts = 16384;  // per-block counts scanned in LDS up to 64 KiB
 constexpr int kPermRounds = kPermSlotsPerBlock / kPermThreads;
 
 __global__ __launch_bounds__(kPermThreads) void perm_count_kernel(const int32_t *__restrict__ ids,
@@ -57,12 +58,22 @@ __global__ __launch_bounds__(kPermThreads) void perm_scan_kernel(
   __shared__ int t0[kMaxExperts + 2];
   __shared__ int t1[kMaxExperts + 2];
   __shared__ int tmp[kPermThreads];
+  // The per-block counts are scanned in LDS when they fit (one coalesced read
+  // and one write): a per-expert walk over the blocks in global memory is a
+  // chain of nblk dependent load/store round trips (32 blocks: about 20 us).
+  __shared__ int cl[kScanLdsInts];
+  const bool in_lds = (long long)nblk * N <= kScanLdsInts;
   const int groups = N + (t_shared > 0 ? 1 : 0);
+  if (in_lds) {
+    for (int i = threadIdx.x; i < nblk * N; i += kPermThreads) cl[i] = blk_counts[i];
+    __syncthreads();
+  }
   for (int e = threadIdx.x; e < N; e += kPermThreads) {
     int running = 0;
     for (int b = 0; b < nblk; ++b) {
-      const int c = blk_counts[(size_t)b * N + e];
-      blk_counts[(size_t)b * N + e] = running;
+      int *slot = in_lds ? &cl[b * N + e] : &blk_counts[(size_t)b * N + e];
+      const int c = *slot;
+      *slot = running;
       running += c;
     }
     tot[e] = running;
@@ -77,9 +88,12 @@ __global__ __launch_bounds__(kPermThreads) void perm_scan_kernel(
   const int n_t0 = block_exclusive_scan(t0, groups, tmp);
   const int n_t1 = block_exclusive_scan(t1, groups, tmp);
   block_exclusive_scan(tot, N, tmp);
-  for (int e = threadIdx.x; e < N; e += kPermThreads) {
-    offsets[e] = tot[e];
-    for (int b = 0; b < nblk; ++b) blk_counts[(size_t)b * N + e] += tot[e];
+  for (int e = threadIdx.x; e < N; e += kPermThreads) offsets[e] = tot[e];
+  if (in_lds) {
+    for (int i = threadIdx.x; i < nblk * N; i += kPermThreads) blk_counts[i] = cl[i] + tot[i % N];
+  } else {
+    for (int e = threadIdx.x; e < N; e += kPermThreads)
+      for (int b = 0; b < nblk; ++b) blk_counts[(size_t)b * N + e] += tot[e];
   }
   for (int g = threadIdx.x; g < groups; g += kPermThreads) {
     tile_start0[g] = t0[g];
