@@ -309,6 +309,32 @@ exfold_status exfold_calibrate_projectors(const exfold_layer *layer, const void 
 /* Static text for a status code. */
 const char *exfold_status_str(exfold_status status);
 
+/* Kernel families of the expert GEMMs (exfold_gemm_plan). */
+enum {
+  EXFOLD_GEMM_SIMT = 0,    /* float32 layers                                          */
+  EXFOLD_GEMM_TILE = 1,    /* 128x128 MFMA tiles                                      */
+  EXFOLD_GEMM_SKINNY = 2,  /* 32x64 tiles streaming weights (few rows per expert)     */
+  EXFOLD_GEMM_WIDE = 3     /* 256x256 tiles (128x512 tails) in rounds of one per CU   */
+};
+
+/*
+ * Host-only query of the expert-GEMM plan the library takes for `rows`
+ * executed rows (routed slots plus shared-expert rows) of a layer, when about
+ * `active_groups` expert groups are non-empty, on a device with `cu_count`
+ * compute units (the forward uses the device's count).  No device call.
+ * out[10] = { gate_up: kind, bm, bn, ksplit, grid,  down: kind, bm, bn, ksplit, grid }
+ * (kind an EXFOLD_GEMM_* value; bm the tile height, or for EXFOLD_GEMM_WIDE the
+ * 128-row unit of its tile list; bn the tile width in output columns, or
+ * weight rows for gate/up; grid the workgroups launched, an upper bound on the
+ * tiles any split of the rows into groups can produce, plus for
+ * EXFOLD_GEMM_WIDE one round for the split remainder).  The forward drops the
+ * down split (ksplit 1) when each token owns one row or the rows are kept.
+ * Errors: the layer's validation codes; EXFOLD_ERR_NULL for out == NULL;
+ * EXFOLD_ERR_SHAPE for rows < 0, active_groups < 1 or cu_count < 1.
+ */
+exfold_status exfold_gemm_plan(const exfold_layer *layer, int64_t rows, int64_t active_groups,
+                               int32_t cu_count, int32_t *out);
+
 /*
  * Diagonal projector calibration (Appendix A, Eq. appendix_diagonal_projector;
  * the unfused family of the projector ablation).  Routing, evaluated pairs and

@@ -638,4 +638,30 @@ exfold_status exfold_calibrate_diagonal(const exfold_layer *layer, const void *x
   return EXFOLD_OK;
 }
 
+static_assert(EXFOLD_GEMM_SIMT == kGemmSimt && EXFOLD_GEMM_TILE == kGemmTile &&
+                  EXFOLD_GEMM_SKINNY == kGemmSkinny && EXFOLD_GEMM_WIDE == kGemmWide,
+              "the header's GEMM kinds are the planner's");
+
+exfold_status exfold_gemm_plan(const exfold_layer *L, int64_t rows, int64_t active_groups,
+                               int32_t cu_count, int32_t *out) {
+  exfold_status st = check_layer(L);
+  if (st != EXFOLD_OK) return st;
+  if (!out) return EXFOLD_ERR_NULL;
+  if (rows < 0 || rows > (int64_t)kMaxSlots + kMaxTokens || active_groups < 1 || cu_count < 1)
+    return EXFOLD_ERR_SHAPE;
+  const int groups = (int)L->n_experts + (L->shared_inter > 0 ? 1 : 0);
+  GemmPlan gu, dn;
+  plan_expert_gemms(L->dtype, (int)rows, groups, (int)(active_groups < groups ? active_groups : groups),
+                    (int)L->d, (int)L->inter, cu_count, &gu, &dn);
+  const GemmPlan *pl[2] = {&gu, &dn};
+  for (int i = 0; i < 2; ++i) {
+    out[5 * i + 0] = pl[i]->kind;
+    out[5 * i + 1] = pl[i]->bm;
+    out[5 * i + 2] = pl[i]->bn;
+    out[5 * i + 3] = pl[i]->ksplit;
+    out[5 * i + 4] = pl[i]->grid;
+  }
+  return EXFOLD_OK;
+}
+
 }  // extern "C"

@@ -27,7 +27,7 @@ EXPORTED = [
     "exfold_moe_workspace_size", "exfold_moe_forward", "exfold_execute_workspace_size",
     "exfold_moe_execute", "exfold_calibrate_workspace_size", "exfold_calibrate_projectors",
     "exfold_calibrate_diagonal",
-    "exfold_status_str",
+    "exfold_status_str", "exfold_gemm_plan",
 ]
 
 
@@ -96,6 +96,7 @@ def lib() -> ctypes.CDLL:
             "exfold_calibrate_projectors": (i32, [vp, vp, i64, dbl, dbl, i32, vp, vp, vp, vp, vp, sz, vp]),
             "exfold_calibrate_diagonal": (i32, [vp, vp, i64, dbl, i32, vp, vp, vp, sz, vp]),
             "exfold_status_str": (ctypes.c_char_p, [i32]),
+            "exfold_gemm_plan": (i32, [vp, i64, i64, i32, vp]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
