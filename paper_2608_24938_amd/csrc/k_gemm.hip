@@ -331,7 +331,12 @@ __device__ __forceinline__ uint32_t lds_addr(const void *ptr) {
 
 // One 16-byte chunk per lane from global g into the 1 KiB LDS block at byte
 // address lds (wave-uniform): lane l lands at lds + 16 l.  M0 holds the block
-// address; one wait state separates its write from the load.
+// address; one wait state separates its write from the load.  The statement
+// clobbers M0, which the compiler does not save around it: the kernels that
+// use it must give the compiler no reason to hold a value in M0 (register
+// arrays indexed by compile-time constants only, no indirect register moves).
+// The compiler's own LDS-DMA builtin keeps M0 safe but schedules the main loop
+// 2% slower (its conservative waits).
 __device__ __forceinline__ void lds_dma16(const void *g, uint32_t lds) {
   asm volatile("s_mov_b32 m0, %1\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %0, off"
                :
