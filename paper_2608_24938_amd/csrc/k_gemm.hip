@@ -604,6 +604,70 @@ __device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, 
   }
 }
 
+// Finished bf16 tile through LDS (the ring is free after the main loop): each
+// lane writes its runs of four columns (SiLU(gate) * up, or the down output
+// times the row's routing weight) into a row-major bf16 tile, and the
+// workgroup then stores whole rows 16 bytes a lane, so one store instruction
+// covers a few complete rows instead of 32 scattered 16-byte pieces.  Taken
+// for the bf16 rows of the down projection (Qwen3-shaped prefill: down 200 ->
+// 177 us); for H and the direct y it cost more than it saved (the extra path
+// spills scalar registers in those kernels).
+template <bool GATE_UP, bool DIRECT, int NW, bool DBL>
+__device__ __forceinline__ void wide_store_lds(const GemmKArgs &p, const TileId &t, int row0, int valid,
+                                               const f32x16 (&acc)[kWideTM][kWideTN], bf16_t *smem) {
+  constexpr int WN = DBL ? NW : NW / 2, TN = kWideTN, BM = DBL ? kWide / 2 : kWide;
+  constexpr int COLS = (GATE_UP ? 16 : 32) * TN * WN;        // output columns of the tile
+  constexpr int PITCH = COLS * 2 + 16;                        // LDS bytes per row (padded)
+  static_assert(BM * PITCH <= kWideSmemElems * 2, "staging tile fits the ring");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int wm = wave / WN, wn = wave % WN;
+  const int c4 = 4 * (lane >> 5);
+  char *lds = reinterpret_cast<char *>(smem);
+#pragma unroll
+  for (int i = 0; i < kWideTM; ++i) {
+    const int ml = wm * 128 + i * 32 + (lane & 31);
+    const float w = (!GATE_UP && ml < valid) ? p.row_w[row0 + ml] : 1.f;
+    char *rowp = lds + ml * PITCH;
+    if (GATE_UP) {
+#pragma unroll
+      for (int j = 0; j < TN / 2; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x16 &gt = acc[i][j], &up = acc[i][j + TN / 2];
+          store4_bf16(reinterpret_cast<bf16_t *>(rowp) + wn * 16 * TN + j * 32 + 8 * g + c4,
+                      silu(gt[4 * g]) * up[4 * g], silu(gt[4 * g + 1]) * up[4 * g + 1],
+                      silu(gt[4 * g + 2]) * up[4 * g + 2], silu(gt[4 * g + 3]) * up[4 * g + 3]);
+        }
+    } else {
+#pragma unroll
+      for (int j = 0; j < TN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const f32x16 &c = acc[i][j];
+          store4_bf16(reinterpret_cast<bf16_t *>(rowp) + wn * 32 * TN + j * 32 + 8 * g + c4, c[4 * g] * w,
+                      c[4 * g + 1] * w, c[4 * g + 2] * w, c[4 * g + 3] * w);
+        }
+    }
+  }
+  lds_barrier();
+  constexpr int CPR = COLS / 8;                               // 16-byte chunks per row
+  for (int q = threadIdx.x; q < BM * CPR; q += 64 * NW) {
+    const int ml = q / CPR, ch = q % CPR;
+    if (ml >= valid) continue;
+    const int row = row0 + ml;
+    const u32x4 v = *reinterpret_cast<const u32x4 *>(lds + ml * PITCH + ch * 16);
+    bf16_t *dst;
+    if (GATE_UP)
+      dst = p.H + (long long)row * p.inter + t.nt * (kWideBN / 2);
+    else if (DIRECT)
+      dst = p.y + (long long)p.row_token[row] * p.d + t.nt * kWideBN;
+    else
+      dst = p.Yh + (long long)row * p.d + t.nt * kWideBN;
+    *reinterpret_cast<u32x4 *>(dst + ch * 8) = v;
+  }
+}
+
+
 // ---------------------------------------------------------------------------
 // Wide-tile launches: whole rounds of tiles plus a split remainder.  With one
 // workgroup per CU (the ring takes 128 KiB of LDS), tiles run in rounds of G =
@@ -684,6 +748,8 @@ __device__ __forceinline__ void wide_gemm(const GemmKArgs &p, int G, bf16_t *sme
     wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, true>(p, t, row0, valid, k0, k1, smem, acc);
     if (part)
       wide_store_partial<true>(part, acc);
+    else if (!GATE_UP && !DIRECT && p.Yh)
+      wide_store_lds<GATE_UP, DIRECT, NW, true>(p, t, row0, valid, acc, smem);
     else
       wide_store<GATE_UP, DIRECT, NW, true>(p, t, row0, valid, acc);
   } else {
@@ -691,6 +757,8 @@ __device__ __forceinline__ void wide_gemm(const GemmKArgs &p, int G, bf16_t *sme
     wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, false>(p, t, row0, valid, k0, k1, smem, acc);
     if (part)
       wide_store_partial<false>(part, acc);
+    else if (!GATE_UP && !DIRECT && p.Yh)
+      wide_store_lds<GATE_UP, DIRECT, NW, false>(p, t, row0, valid, acc, smem);
     else
       wide_store<GATE_UP, DIRECT, NW, false>(p, t, row0, valid, acc);
   }
