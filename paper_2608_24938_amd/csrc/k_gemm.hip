@@ -1246,29 +1246,35 @@ __global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y,
                                                      int rows, const int32_t *__restrict__ slot_row,
                                                      int k_out, int d, int shared_base,
                                                      OutT *__restrict__ y) {
-  // block (i, c): token i, columns [1024 c, 1024 c + 1024), four per thread
+  // block (i, c): token i, columns [2048 c, 2048 c + 2048), eight per thread
+  // (16-byte loads of bf16 rows and 16-byte bf16 stores)
   const int i = blockIdx.x;
+  const int c = blockIdx.y * 2048 + threadIdx.x * 8;
+  if (c >= d) return;
   const long long split = (long long)rows * d;
-  for (int c = blockIdx.y * 1024 + threadIdx.x * 4; c < min(d, (int)(blockIdx.y + 1) * 1024); c += 1024) {
-    float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int k = 0; k <= k_out; ++k) {
-      long long r;
-      if (k < k_out)
-        r = slot_row[(long long)i * k_out + k];
-      else if (shared_base >= 0)
-        r = shared_base + i;
-      else
-        break;
-      for (int sp = 0; sp < ksplit; ++sp) {
-        const float4 v = load4<InT>(Y + sp * split + r * d + c);
-        acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
-      }
+  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  for (int k = 0; k <= k_out; ++k) {
+    long long r;
+    if (k < k_out)
+      r = slot_row[(long long)i * k_out + k];
+    else if (shared_base >= 0)
+      r = shared_base + i;
+    else
+      break;
+    for (int sp = 0; sp < ksplit; ++sp) {
+      const InT *src = Y + sp * split + r * d + c;
+      const float4 v0 = load4<InT>(src), v1 = load4<InT>(src + 4);
+      acc[0] += v0.x; acc[1] += v0.y; acc[2] += v0.z; acc[3] += v0.w;
+      acc[4] += v1.x; acc[5] += v1.y; acc[6] += v1.z; acc[7] += v1.w;
     }
-    OutT *o = y + (long long)i * d + c;
-    o[0] = store_cvt<OutT>(acc.x);
-    o[1] = store_cvt<OutT>(acc.y);
-    o[2] = store_cvt<OutT>(acc.z);
-    o[3] = store_cvt<OutT>(acc.w);
+  }
+  OutT *o = y + (long long)i * d + c;
+  if constexpr (sizeof(OutT) == 2) {
+    store4_bf16(reinterpret_cast<bf16_t *>(o), acc[0], acc[1], acc[2], acc[3]);
+    store4_bf16(reinterpret_cast<bf16_t *>(o) + 4, acc[4], acc[5], acc[6], acc[7]);
+  } else {
+    *reinterpret_cast<float4 *>(o) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    *reinterpret_cast<float4 *>(o + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
   }
 }
 
@@ -1276,7 +1282,7 @@ hipError_t launch_combine(int dtype, const float *Y, bool y_bf16, int ksplit, in
                           const int32_t *slot_row, int T, int k_out, int d, int shared_base, void *y,
                           hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  const dim3 grid(T, (d + 1023) / 1024);
+  const dim3 grid(T, (d + 2047) / 2048);
   if (dtype == EXFOLD_BF16 && y_bf16)
     combine_kernel<bf16_t, bf16_t><<<grid, 256, 0, s>>>(reinterpret_cast<const bf16_t *>(Y), ksplit,
                                                         rows, slot_row, k_out, d, shared_base,
