@@ -794,15 +794,22 @@ __global__ __launch_bounds__(256) void expert_wide_fixup(const GemmKArgs p, int 
   if (ml >= valid) return;
   const int row = row0 + ml;
   const float *P0 = p.P + (size_t)r * w.s * kWideTileElems + (size_t)ml * bn;
+  // all s partials of a column group are loaded before the in-order sum (the
+  // loads do not wait on each other)
   auto sum4 = [&](int col) {
+    float4 q[kWideMaxSplit];
+#pragma unroll
+    for (int k = 0; k < kWideMaxSplit; ++k)
+      if (k < w.s) q[k] = *reinterpret_cast<const float4 *>(P0 + (size_t)k * kWideTileElems + col);
     float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-    for (int k = 0; k < w.s; ++k) {
-      const float4 q = *reinterpret_cast<const float4 *>(P0 + (size_t)k * kWideTileElems + col);
-      v.x += q.x;
-      v.y += q.y;
-      v.z += q.z;
-      v.w += q.w;
-    }
+#pragma unroll
+    for (int k = 0; k < kWideMaxSplit; ++k)
+      if (k < w.s) {
+        v.x += q[k].x;
+        v.y += q[k].y;
+        v.z += q[k].z;
+        v.w += q[k].w;
+      }
     return v;
   };
   if (GATE_UP) {
