@@ -110,6 +110,47 @@ __device__ __forceinline__ void lds_barrier() {
 
 __device__ __forceinline__ uint64_t lanemask_lt(int lane) { return (lane == 0) ? 0ull : (~0ull >> (64 - lane)); }
 
+// Exclusive prefix sums of three per-thread counts over the first kW waves of
+// the workgroup, thread i holding element i of each sequence: a scan inside
+// each wave, then the wave totals through LDS (`part`, 3 * kW ints).  Every
+// thread of the workgroup calls it (it holds one LDS barrier).  Threads of the
+// first kW waves get their exclusive prefixes in ex; every thread gets the
+// totals in tot.
+template <int kW>
+__device__ __forceinline__ void block_scan3(const int (&v)[3], int (&ex)[3], int (&tot)[3], int *part) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  int in[3] = {v[0], v[1], v[2]};
+  if (wave < kW) {
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+      int x[3];
+#pragma unroll
+      for (int q = 0; q < 3; ++q) x[q] = __shfl_up(in[q], off, 64);
+      if (lane >= off) {
+#pragma unroll
+        for (int q = 0; q < 3; ++q) in[q] += x[q];
+      }
+    }
+    if (lane == 63) {
+#pragma unroll
+      for (int q = 0; q < 3; ++q) part[q * kW + wave] = in[q];
+    }
+  }
+  lds_barrier();
+#pragma unroll
+  for (int q = 0; q < 3; ++q) {
+    int pre = 0, all = 0;
+#pragma unroll
+    for (int w = 0; w < kW; ++w) {
+      const int sw = part[q * kW + w];
+      pre += (w < wave) ? sw : 0;
+      all += sw;
+    }
+    ex[q] = pre + in[q] - v[q];
+    tot[q] = all;
+  }
+}
+
 // XCD-aware remap of a workgroup id: the hardware deals consecutive workgroup
 // ids round-robin over the 8 XCDs; this returns a logical id such that every
 // XCD works on one contiguous range of logical ids (tiles that share operands

@@ -28,84 +28,77 @@ __global__ __launch_bounds__(kPermThreads) void perm_count_kernel(const int32_t 
   for (int e = threadIdx.x; e < N; e += kPermThreads) blk_counts[(size_t)blockIdx.x * N + e] = cnt[e];
 }
 
-// Exclusive scan of buf[0..n) (n <= 2 * kPermThreads) in LDS; returns the total.
-__device__ int block_exclusive_scan(int *buf, int n, int *tmp) {
-  const int t = threadIdx.x;
-  const int a = (2 * t < n) ? buf[2 * t] : 0;
-  const int b = (2 * t + 1 < n) ? buf[2 * t + 1] : 0;
-  tmp[t] = a + b;
-  __syncthreads();
-  for (int off = 1; off < kPermThreads; off <<= 1) {
-    const int v = (t >= off) ? tmp[t - off] : 0;
-    __syncthreads();
-    tmp[t] += v;
-    __syncthreads();
-  }
-  const int excl = tmp[t] - (a + b);
-  const int total = tmp[kPermThreads - 1];
-  __syncthreads();
-  if (2 * t < n) buf[2 * t] = excl;
-  if (2 * t + 1 < n) buf[2 * t + 1] = excl + a;
-  __syncthreads();
-  return total;
-}
+// One thread per group in the scan kernel: kScanWaves waves cover the
+// kMaxExperts + 1 groups (routed experts, shared expert).
+constexpr int kScanWaves = (kMaxExperts + 1 + kWave - 1) / kWave;
+constexpr int kScanThreads = kScanWaves * kWave;
 
-__global__ __launch_bounds__(kPermThreads) void perm_scan_kernel(
+__global__ __launch_bounds__(kScanThreads) void perm_scan_kernel(
     int32_t *__restrict__ blk_counts, int nblk, int N, int R, int t_shared, int bm0, int bm1,
     int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start0,
     int32_t *__restrict__ tile_start1) {
-  __shared__ int tot[kMaxExperts + 2];
-  __shared__ int t0[kMaxExperts + 2];
-  __shared__ int t1[kMaxExperts + 2];
-  __shared__ int tmp[kPermThreads];
+  __shared__ int part[3 * kScanWaves];
+  __shared__ int off_sh[kMaxExperts];
   // The per-block counts are scanned in LDS when they fit (one coalesced read
   // and one write): a per-expert walk over the blocks in global memory is a
   // chain of nblk dependent load/store round trips (32 blocks: about 20 us).
   __shared__ int cl[kScanLdsInts];
+  const int tid = threadIdx.x;
   const bool in_lds = (long long)nblk * N <= kScanLdsInts;
   const int groups = N + (t_shared > 0 ? 1 : 0);
   if (in_lds) {
-    for (int i = threadIdx.x; i < nblk * N; i += kPermThreads) cl[i] = blk_counts[i];
-    __syncthreads();
+    for (int i = tid; i < nblk * N; i += kScanThreads) cl[i] = blk_counts[i];
+    lds_barrier();
   }
-  for (int e = threadIdx.x; e < N; e += kPermThreads) {
-    int running = 0;
-    for (int b = 0; b < nblk; ++b) {
-      int *slot = in_lds ? &cl[b * N + e] : &blk_counts[(size_t)b * N + e];
-      const int c = *slot;
-      *slot = running;
-      running += c;
+  // Thread e: exclusive scan of expert e's counts over the blocks, in block
+  // order; the counts are read eight blocks at a time.
+  int total = 0;
+  if (tid < N) {
+    constexpr int kB = 8;
+    int *base = in_lds ? cl : blk_counts;
+    int b = 0;
+    for (; b + kB <= nblk; b += kB) {
+      int c[kB];
+#pragma unroll
+      for (int q = 0; q < kB; ++q) c[q] = base[(size_t)(b + q) * N + tid];
+#pragma unroll
+      for (int q = 0; q < kB; ++q) {
+        base[(size_t)(b + q) * N + tid] = total;
+        total += c[q];
+      }
     }
-    tot[e] = running;
+    for (; b < nblk; ++b) {
+      const int c = base[(size_t)b * N + tid];
+      base[(size_t)b * N + tid] = total;
+      total += c;
+    }
   }
-  if (threadIdx.x == 0) tot[N] = t_shared;
-  __syncthreads();
-  for (int g = threadIdx.x; g < groups; g += kPermThreads) {
-    t0[g] = (tot[g] + bm0 - 1) / bm0;
-    t1[g] = (tot[g] + bm1 - 1) / bm1;
+  // Group g: rows, m-tiles of height bm0 and bm1; exclusive scans over groups.
+  int v[3] = {0, 0, 0};
+  if (tid < groups) {
+    const int r = tid < N ? total : t_shared;
+    v[0] = r;
+    v[1] = (r + bm0 - 1) / bm0;
+    v[2] = (r + bm1 - 1) / bm1;
   }
-  __syncthreads();
-  const int n_t0 = block_exclusive_scan(t0, groups, tmp);
-  const int n_t1 = block_exclusive_scan(t1, groups, tmp);
-  block_exclusive_scan(tot, N, tmp);
-  for (int e = threadIdx.x; e < N; e += kPermThreads) offsets[e] = tot[e];
+  int ex[3], tot[3];
+  block_scan3<kScanWaves>(v, ex, tot, part);
+  if (tid < N) {
+    offsets[tid] = ex[0];
+    off_sh[tid] = ex[0];
+  }
+  if (tid == N) offsets[N] = R;
+  if (tid == N + 1) offsets[N + 1] = R + t_shared;
+  if (tid < N + 2) {
+    tile_start0[tid] = tid < groups ? ex[1] : tot[1];
+    tile_start1[tid] = tid < groups ? ex[2] : tot[2];
+  }
+  // Per-block bases: the block's exclusive prefix plus the group offset.
   if (in_lds) {
-    for (int i = threadIdx.x; i < nblk * N; i += kPermThreads) blk_counts[i] = cl[i] + tot[i % N];
-  } else {
-    for (int e = threadIdx.x; e < N; e += kPermThreads)
-      for (int b = 0; b < nblk; ++b) blk_counts[(size_t)b * N + e] += tot[e];
-  }
-  for (int g = threadIdx.x; g < groups; g += kPermThreads) {
-    tile_start0[g] = t0[g];
-    tile_start1[g] = t1[g];
-  }
-  if (threadIdx.x == 0) {
-    offsets[N] = R;
-    offsets[N + 1] = R + t_shared;
-    for (int g = groups; g < N + 2; ++g) {
-      tile_start0[g] = n_t0;
-      tile_start1[g] = n_t1;
-    }
+    lds_barrier();
+    for (int i = tid; i < nblk * N; i += kScanThreads) blk_counts[i] = cl[i] + off_sh[i % N];
+  } else if (tid < N) {
+    for (int b = 0; b < nblk; ++b) blk_counts[(size_t)b * N + tid] += ex[0];
   }
 }
 
@@ -172,7 +165,7 @@ hipError_t launch_permute(const int32_t *route_ids, const float *route_w, int T,
   const int R = T * k_out;
   const int nblk = (R + kPermSlotsPerBlock - 1) / kPermSlotsPerBlock;
   if (nblk > 0) perm_count_kernel<<<nblk, kPermThreads, 0, s>>>(route_ids, R, N, pb.blk_counts);
-  perm_scan_kernel<<<1, kPermThreads, 0, s>>>(pb.blk_counts, nblk, N, R, t_shared, bm0, bm1,
+  perm_scan_kernel<<<1, kScanThreads, 0, s>>>(pb.blk_counts, nblk, N, R, t_shared, bm0, bm1,
                                               pb.offsets, pb.tile_start0, pb.tile_start1);
   if (nblk > 0)
     perm_scatter_kernel<<<nblk, kPermThreads, 0, s>>>(route_ids, route_w, R, k_out, N, t_shared,

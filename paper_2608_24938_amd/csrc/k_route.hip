@@ -17,27 +17,28 @@ namespace exfold {
 // ---------------------------------------------------------------------------
 // Router logits, as P partial sums over slices of d (the bias and the sum of the
 // partials are taken by the Top-K kernel, in a fixed order).  bf16: workgroup
-// (bx, by, bz) takes 16 tokens x NT*16 experts x one d-slice; its KS waves split
-// the slice, reduce with 16x16x32 bf16 MFMA and add their partial sums in a fixed
-// order through LDS.  Many tokens: one block covers every expert (W_r is read
-// once per 16 tokens); few tokens: 16 experts per block and the d axis split
+// (bx, by, bz) takes 16*TT tokens x NT*16 experts x one d-slice; its KS waves
+// split the slice, reduce with 16x16x32 bf16 MFMA (each weight fragment feeds TT
+// token groups) and add their partial sums in a fixed order through LDS.  Many
+// tokens: one block covers every expert (W_r is read once per 16*TT tokens); few tokens: 16 experts per block and the d axis split
 // over the grid, so the small GEMM still spreads over the CUs.
 // f32: one thread per logit.
 // ---------------------------------------------------------------------------
-template <int NT, int KS>
+template <int NT, int KS, int TT = 1>
 __global__ __launch_bounds__(64 * KS) void router_logits_bf16(const bf16_t *__restrict__ x,
                                                               const bf16_t *__restrict__ wr,
                                                               int T, int N, int d, int d_slice,
                                                               float *__restrict__ part) {
-  __shared__ float red[KS][NT * 4][64];
+  __shared__ float red[KS][TT * NT * 4][64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  const int t0 = blockIdx.x * 16;
+  const int t0 = blockIdx.x * 16 * TT;
   const int e0 = blockIdx.y * NT * 16;
-  const int row = min(t0 + (lane & 15), T - 1);
   const int kq = (lane >> 4) * 8 + blockIdx.z * d_slice;
-  f32x4 acc[NT];
+  f32x4 acc[TT][NT];
 #pragma unroll
-  for (int j = 0; j < NT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  for (int u = 0; u < TT; ++u)
+#pragma unroll
+    for (int j = 0; j < NT; ++j) acc[u][j] = f32x4{0.f, 0.f, 0.f, 0.f};
   const bf16_t *wrow[NT];
   bool live[NT];
 #pragma unroll
@@ -46,52 +47,64 @@ __global__ __launch_bounds__(64 * KS) void router_logits_bf16(const bf16_t *__re
     live[j] = e < N;
     wrow[j] = wr + (size_t)(live[j] ? e : 0) * d + kq;
   }
-  const bf16_t *xa = x + (size_t)row * d + kq;
+  const bf16_t *xa[TT];
+#pragma unroll
+  for (int u = 0; u < TT; ++u) xa[u] = x + (size_t)min(t0 + u * 16 + (lane & 15), T - 1) * d + kq;
   const int steps = d_slice / 32;
   const int s0 = wave * steps / KS, s1 = (wave + 1) * steps / KS;
+  const int npair = (s1 - s0) / 2;
   bf16x8 zero;
 #pragma unroll
   for (int q = 0; q < 8; ++q) zero[q] = (__bf16)0.0f;
-  int st = s0;
-  for (; st + 2 <= s1; st += 2) {
-    const int k = st * 32;
-    const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(xa + k);
-    const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(xa + k + 32);
-    bf16x8 b0[NT], b1[NT];
+  for (int i = 0; i < npair; ++i) {
+    const int k = (s0 + 2 * i) * 32;
+    bf16x8 a0[TT], a1[TT], b0[NT], b1[NT];
+#pragma unroll
+    for (int u = 0; u < TT; ++u) {
+      a0[u] = *reinterpret_cast<const bf16x8 *>(xa[u] + k);
+      a1[u] = *reinterpret_cast<const bf16x8 *>(xa[u] + k + 32);
+    }
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       b0[j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
       b1[j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k + 32);
     }
 #pragma unroll
-    for (int j = 0; j < NT; ++j) {
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, live[j] ? b0[j] : zero, acc[j], 0, 0, 0);
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, live[j] ? b1[j] : zero, acc[j], 0, 0, 0);
-    }
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int u = 0; u < TT; ++u) {
+        acc[u][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[u], live[j] ? b0[j] : zero, acc[u][j], 0, 0, 0);
+        acc[u][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1[u], live[j] ? b1[j] : zero, acc[u][j], 0, 0, 0);
+      }
   }
-  if (st < s1) {
-    const int k = st * 32;
-    const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(xa + k);
+  if ((s1 - s0) & 1) {
+    const int k = (s1 - 1) * 32;
+    bf16x8 a0[TT];
+#pragma unroll
+    for (int u = 0; u < TT; ++u) a0[u] = *reinterpret_cast<const bf16x8 *>(xa[u] + k);
 #pragma unroll
     for (int j = 0; j < NT; ++j) {
       const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
-      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, live[j] ? b0 : zero, acc[j], 0, 0, 0);
+#pragma unroll
+      for (int u = 0; u < TT; ++u)
+        acc[u][j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0[u], live[j] ? b0 : zero, acc[u][j], 0, 0, 0);
     }
   }
 #pragma unroll
-  for (int j = 0; j < NT; ++j)
+  for (int u = 0; u < TT; ++u)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) red[wave][j * 4 + i][lane] = acc[j][i];
+    for (int j = 0; j < NT; ++j)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) red[wave][(u * NT + j) * 4 + i][lane] = acc[u][j][i];
   __syncthreads();
-  // entry (j, i, l): expert e0 + j*16 + l%16, token t0 + (l/16)*4 + i
   float *out = part + (size_t)blockIdx.z * T * N;
-  for (int idx = threadIdx.x; idx < NT * 4 * 64; idx += 64 * KS) {
+  for (int idx = threadIdx.x; idx < TT * NT * 4 * 64; idx += 64 * KS) {
     const int ji = idx >> 6, l = idx & 63;
-    const int j = ji >> 2, i = ji & 3;
+    const int u = ji / (NT * 4), j = (ji >> 2) % NT, i = ji & 3;
     float v = red[0][ji][l];
 #pragma unroll
     for (int w = 1; w < KS; ++w) v += red[w][ji][l];
-    const int t = t0 + (l >> 4) * 4 + i;
+    const int t = t0 + u * 16 + (l >> 4) * 4 + i;
     const int e = e0 + j * 16 + (l & 15);
     if (t < T && e < N) out[(size_t)t * N + e] = v;
   }
@@ -114,6 +127,13 @@ int router_splits(int dtype, int T, int N, int d) {
 template <int NT>
 static void launch_router_wide(const bf16_t *x, const bf16_t *wr, int T, int N, int d, float *part,
                                hipStream_t s) {
+  if constexpr (NT >= 4 && NT <= 8) {
+    // 32 tokens per workgroup: each weight row piece is fetched once per 32
+    // tokens; 8192 tokens x 128 experts x 2048 took 43 us with 16 tokens and
+    // four waves, 29 us like this (64 tokens per workgroup: 48 us)
+    router_logits_bf16<NT, 8, 2><<<dim3((T + 31) / 32, 1, 1), 512, 0, s>>>(x, wr, T, N, d, d, part);
+    return;
+  }
   const int blocks = (T + 15) / 16;
   if (blocks < 512)
     router_logits_bf16<NT, 8><<<dim3(blocks, 1, 1), 512, 0, s>>>(x, wr, T, N, d, d, part);
@@ -621,6 +641,14 @@ hipError_t launch_static_pool(const float *h, int N, int D, const float *S, cons
 // the expert GEMMs.  The [B, K] slots stay in LDS after one read.
 // ---------------------------------------------------------------------------
 constexpr int kFrontWaves = kPoolThreads / kWave;
+// Up to this many experts the front end loads each thread's share of L and S
+// with the slots (at most kFrontPfCols entries of each per thread), so the
+// table step does not wait for a load that depends on the pool.  Larger
+// tables load only the pool's columns, after the pool step (prefetching all
+// 128 x 128 entries measured about 2 us slower).
+constexpr int kFrontPfN = 32;
+constexpr int kFrontPfCols = (kFrontPfN * kFrontPfN + kPoolThreads - 1) / kPoolThreads;
+constexpr int kFrontScanWaves = (kMaxExperts + 2 + kWave - 1) / kWave;
 
 __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     const int32_t *__restrict__ ids, const float *__restrict__ w, int B, int N, int K, int D,
@@ -644,6 +672,8 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   __shared__ int rank_sh[kMaxExperts];
   __shared__ int cur[kMaxExperts];
   __shared__ int wcnt[kFrontWaves][kMaxExperts];
+  __shared__ unsigned long long best[kMaxExperts];
+  __shared__ int scan_part[3 * kFrontScanWaves];
   __shared__ int n_pool;
   // Threads hand data to each other through LDS only, and no global output is
   // read back here, so the phase barriers order LDS alone.
@@ -654,7 +684,16 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
 
   const float h_e = (tid < N && h) ? h[tid] : 0.f;
   const bool dynamic = static_tgt == nullptr;  // uniform over the workgroup
+  // Table entries of thread (src, part): L[src, t] and S[src, t] for
+  // t = part, part + P, ... (N <= kFrontPfN, so at most kFrontPfCols of each),
+  // loaded once the slots are in (loads complete in issue order, so loading
+  // them first would hold up the slots) and used after the pool step.
+  const bool pf = dynamic && N <= kFrontPfN;
+  const int P = kPoolThreads / N;
+  const int src = tid / P, part = tid % P;
+  float lv[kFrontPfCols], sv[kFrontPfCols];
   if (tid < N) {
+    best[tid] = ~0ull;
     wsum[tid] = 0ull;
     cnt[tid] = 0;
     in_pool[tid] = 0;
@@ -681,6 +720,13 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
       atomicAdd(&wsum[e], (unsigned long long)q);
       atomicAdd(&cnt[e], 1);
     }
+  }
+#pragma unroll
+  for (int b = 0; b < kFrontPfCols; ++b) {
+    const int t = part + b * P;
+    const bool ok = pf && src < N && t < N;
+    lv[b] = ok ? L[(size_t)src * N + t] : 0.f;
+    sv[b] = ok ? S[(size_t)src * N + t] : 0.f;
   }
   lds_barrier();
   if (dynamic) {
@@ -713,7 +759,46 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   if (tid == 0) *pool_size_g = n_pool;
 
   // ---- per-source tables (Eq. minimum_loss_assignment over the pool) ----
-  pool_tables(N, S, L, pool, in_pool, n_pool, tgt, scl, tgt_g, scl_g);
+  if (pf) {
+    // the same first minimum in pool order as pool_tables, on the entries
+    // loaded at the start: key (L value, pool position), the pool position of
+    // a member t being its rank
+    uint64_t key = ~0ull;
+    float s_key = 1.0f;
+    if (src < N && !in_pool[src]) {
+#pragma unroll
+      for (int b = 0; b < kFrontPfCols; ++b) {
+        const int t = part + b * P;
+        if (t < N && in_pool[t]) {
+          const uint64_t k = (uint64_t(float_key(lv[b])) << 32) | uint64_t(uint32_t(rank_sh[t]));
+          if (k < key) {
+            key = k;
+            s_key = sv[b];
+          }
+        }
+      }
+      if (key != ~0ull) atomicMin(&best[src], (unsigned long long)key);
+    }
+    lds_barrier();
+    if (src < N) {
+      int t_out = -1;
+      float s_out = 1.0f;
+      if (in_pool[src] || n_pool == 0) {
+        if (part == 0) t_out = src;  // maps to itself
+      } else if (key != ~0ull && key == best[src]) {
+        t_out = pool[(int)(key & 0xffffffffu)];
+        s_out = s_key;
+      }
+      if (t_out >= 0) {
+        tgt[src] = t_out;
+        scl[src] = s_out;
+        if (tgt_g) tgt_g[src] = t_out;
+        if (scl_g) scl_g[src] = s_out;
+      }
+    }
+  } else {
+    pool_tables(N, S, L, pool, in_pool, n_pool, tgt, scl, tgt_g, scl_g);
+  }
   }  // dynamic
   lds_barrier();
 
@@ -731,53 +816,27 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   }
   lds_barrier();
 
-  // ---- group offsets and GEMM m-tile lists: wave 0, five groups per lane ----
-  if (wave == 0) {
-    constexpr int G = 5;  // 64 * 5 >= kMaxExperts + 1 groups
-    int r[G], a[G], b[G];
-    int sr = 0, sa = 0, sb = 0;
-#pragma unroll
-    for (int q = 0; q < G; ++q) {
-      const int g = lane * G + q;
-      r[q] = (g < N) ? rows_of[g] : (g == N && g < groups) ? t_shared : 0;
-      a[q] = g < groups ? (r[q] + bm0 - 1) / bm0 : 0;
-      b[q] = g < groups ? (r[q] + bm1 - 1) / bm1 : 0;
-      sr += r[q];
-      sa += a[q];
-      sb += b[q];
+  // ---- group offsets and GEMM m-tile lists: one group per thread ----
+  {
+    int v[3] = {0, 0, 0};
+    if (tid < groups) {
+      const int r = tid < N ? rows_of[tid] : t_shared;
+      v[0] = r;
+      v[1] = (r + bm0 - 1) / bm0;
+      v[2] = (r + bm1 - 1) / bm1;
     }
-    // exclusive prefix over lanes
-    int er = sr, ea = sa, eb = sb;
+    for (int e = tid; e < N; e += kPoolThreads) {
 #pragma unroll
-    for (int off = 1; off < kWave; off <<= 1) {
-      const int xr = __shfl_up(er, off, kWave), xa = __shfl_up(ea, off, kWave), xb = __shfl_up(eb, off, kWave);
-      if (lane >= off) {
-        er += xr;
-        ea += xa;
-        eb += xb;
-      }
+      for (int q = 0; q < kFrontWaves; ++q) wcnt[q][e] = 0;
     }
-    er -= sr;
-    ea -= sa;
-    eb -= sb;
-    const int ta = (int)readlane_u32((uint32_t)(ea + sa), kWave - 1), tb = (int)readlane_u32((uint32_t)(eb + sb), kWave - 1);
-#pragma unroll
-    for (int q = 0; q < G; ++q) {
-      const int g = lane * G + q;
-      if (g < N) cur[g] = er;  // group start (routed experts)
-      if (g < N + 2) {
-        offsets[g] = (g < N) ? er : (g == N) ? slots : slots + t_shared;
-        tile_start0[g] = (g < groups) ? ea : ta;
-        tile_start1[g] = (g < groups) ? eb : tb;
-      }
-      er += r[q];
-      ea += a[q];
-      eb += b[q];
+    int ex[3], tot[3];
+    block_scan3<kFrontScanWaves>(v, ex, tot, scan_part);
+    if (tid < N) cur[tid] = ex[0];  // group start (routed experts)
+    if (tid < N + 2) {
+      offsets[tid] = (tid < N) ? ex[0] : (tid == N) ? slots : slots + t_shared;
+      tile_start0[tid] = (tid < groups) ? ex[1] : tot[1];
+      tile_start1[tid] = (tid < groups) ? ex[2] : tot[2];
     }
-  }
-  for (int e = tid; e < N; e += kPoolThreads) {
-#pragma unroll
-    for (int q = 0; q < kFrontWaves; ++q) wcnt[q][e] = 0;
   }
   lds_barrier();
 
