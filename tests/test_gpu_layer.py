@@ -55,6 +55,9 @@ def _forward_case(shape, T, phase, budget, seed=2):
     (WIDE_BF16, 500, "prefill", 4), (WIDE_BF16, 64, "decode", 16), (WIDE_BF16, 256, "decode", 32),
     (SHARED_BF16, 100, "prefill", 2), (SHARED_BF16, 48, "decode", 8), (WIDE_F32, 90, "prefill", 3),
     (WIDE_F32, 33, "decode", 5),
+    # 1024+ tokens: the router's many-token layout (32 tokens a workgroup for
+    # 33-128 experts), with a ragged last workgroup
+    (SHARED_BF16, 1100, "prefill", 2), (WIDE_BF16, 1500, "prefill", 4), (SMALL_BF16, 1030, "prefill", 1),
 ])
 def test_forward_matches_oracle(shape, T, phase, budget):
     lp, xs, (S, L, h), dbg, y = _forward_case(shape, T, phase, budget)
