@@ -658,7 +658,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     int bm0, int bm1, int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start0,
     int32_t *__restrict__ tile_start1, int32_t *__restrict__ row_token,
     int32_t *__restrict__ row_slot, float *__restrict__ row_w, int32_t *__restrict__ slot_row,
-    const int32_t *__restrict__ static_tgt, const float *__restrict__ static_scl) {
+    const int32_t *__restrict__ static_tgt, const float *__restrict__ static_scl, int identity) {
   __shared__ uint8_t sid[kDecodeFrontMaxSlots];   // expert of each slot (N <= 256)
   __shared__ float sw[kDecodeFrontMaxSlots];      // its weight
   __shared__ unsigned long long wsum[kMaxExperts];
@@ -683,7 +683,9 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   const int groups = N + (t_shared > 0 ? 1 : 0);
 
   const float h_e = (tid < N && h) ? h[tid] : 0.f;
-  const bool dynamic = static_tgt == nullptr;  // uniform over the workgroup
+  // identity: the permutation alone (every expert maps to itself; out_ids and
+  // out_w unused); else precomputed static tables, else the batch pool
+  const bool dynamic = !identity && static_tgt == nullptr;  // uniform over the workgroup
   // Table entries of thread (src, part): L[src, t] and S[src, t] for
   // t = part, part + P, ... (N <= kFrontPfN, so at most kFrontPfCols of each),
   // loaded once the slots are in (loads complete in issue order, so loading
@@ -699,7 +701,11 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     in_pool[tid] = 0;
     rows_of[tid] = 0;
     rank_sh[tid] = 0;
-    if (!dynamic) {
+    if (identity) {
+      tgt[tid] = tid;
+      scl[tid] = 1.0f;
+      in_pool[tid] = 1;
+    } else if (!dynamic) {
       // precomputed static tables: a source is in the pool iff it maps to itself
       const int te = clamp_id(static_tgt[tid], N);
       tgt[tid] = te;
@@ -808,8 +814,10 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     const float wv = sw[j];
     const int te = tgt[e];
     const float wn = in_pool[e] ? wv : wv * scl[e];
-    out_ids[j] = te;
-    out_w[j] = wn;
+    if (!identity) {
+      out_ids[j] = te;
+      out_w[j] = wn;
+    }
     sid[j] = (uint8_t)te;
     sw[j] = wn;
     atomicAdd(&rows_of[te], 1);
@@ -893,7 +901,18 @@ hipError_t launch_decode_front(const int32_t *ids, const float *w, int B, int N,
                                                  out_w, tgt, scl, t_shared, bm0, bm1, pb.offsets,
                                                  pb.tile_start0, pb.tile_start1, pb.row_token,
                                                  pb.row_slot, pb.row_w, pb.slot_row, static_tgt,
-                                                 static_scl);
+                                                 static_scl, 0);
+  return hipGetLastError();
+}
+
+hipError_t launch_permute_one_block(const int32_t *ids, const float *w, int T, int k_out, int N,
+                                    int t_shared, int bm0, int bm1, const PermBuffers &pb,
+                                    hipStream_t s) {
+  decode_front_kernel<<<1, kPoolThreads, 0, s>>>(ids, w, T, N, k_out, N, nullptr, nullptr, nullptr,
+                                                 nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
+                                                 t_shared, bm0, bm1, pb.offsets, pb.tile_start0,
+                                                 pb.tile_start1, pb.row_token, pb.row_slot, pb.row_w,
+                                                 pb.slot_row, nullptr, nullptr, 1);
   return hipGetLastError();
 }
 

@@ -56,6 +56,12 @@ hipError_t launch_decode_front(const int32_t *ids, const float *w, int B, int N,
                                int32_t *pool_size, int32_t *out_ids, float *out_w, int32_t *tgt,
                                float *scl, int t_shared, int bm0, int bm1, const PermBuffers &pb,
                                const int32_t *static_tgt, const float *static_scl, hipStream_t s);
+// The stable permutation of launch_permute in one workgroup (the decode front
+// end with every expert mapped to itself), for T * k_out <= kDecodeFrontMaxSlots:
+// one launch instead of three.
+hipError_t launch_permute_one_block(const int32_t *ids, const float *w, int T, int k_out, int N,
+                                    int t_shared, int bm0, int bm1, const PermBuffers &pb,
+                                    hipStream_t s);
 // Per-slot remap of [slots] routes with static tables (grid-wide).
 hipError_t launch_static_remap(const int32_t *ids, const float *w, int slots, int N,
                                const int32_t *tgt, const float *scl, int32_t *out_ids, float *out_w,

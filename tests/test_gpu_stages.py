@@ -133,7 +133,9 @@ def test_decode_empty_batch_and_identity():
 
 
 @pytest.mark.parametrize("T,k_out,N,shared", [(64, 1, 8, False), (1000, 4, 128, False), (333, 8, 128, True),
-                                              (1, 2, 8, False), (2500, 3, 256, True), (17, 8, 128, False)])
+                                              (1, 2, 8, False), (2500, 3, 256, True), (17, 8, 128, False),
+                                              # at and just past the one-workgroup capacity (4096 slots)
+                                              (1024, 4, 128, True), (4097, 1, 8, False)])
 def test_permutation_is_stable_counting_sort(T, k_out, N, shared):
     from .gpu_common import LayerPair
     from paper_2608_24938_amd import synth
