@@ -485,15 +485,20 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
                             at<int32_t>(ws, p.o_om_q), at<float>(ws, p.o_wret));
   } else {
     const bool stat = phase == EXFOLD_PHASE_DECODE_STATIC;
-    e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,
-                            topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s);
-    if (e == hipSuccess && (int64_t)p.T * p.K <= kDecodeFrontMaxSlots) {
-      // pool, tables, remap and permutation in one workgroup
+    const bool front = (int64_t)p.T * p.K <= kDecodeFrontMaxSlots;
+    FrontTopK fused;
+    if (front && decode_front_fuses_topk(p.T, p.N))
+      fused = FrontTopK{part, p.P, bias, dbg.logits, topk_ids, topk_w};
+    else
+      e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,
+                              topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s);
+    if (e == hipSuccess && front) {
+      // (Top-K,) pool, tables, remap and permutation in one workgroup
       const PermBuffers pb = perm_buffers(p.ex, ws, dbg.offsets, dbg.row_slot);
       e = launch_decode_front(topk_ids, topk_w, p.T, p.N, p.K, p.dcap, tables->h, tables->S, tables->L,
                               pool, pool_size, fold_ids, fold_w, dbg.tgt_ids, dbg.tgt_scale,
                               p.ex.t_shared, p.ex.gu.bm, p.ex.dn.bm, pb, stat ? tables->tgt : nullptr,
-                              stat ? tables->scl : nullptr, s);
+                              stat ? tables->scl : nullptr, s, fused);
       permuted = true;
     } else if (e == hipSuccess && stat) {
       e = launch_static_remap(topk_ids, topk_w, p.T * p.K, p.N, tables->tgt, tables->scl, fold_ids,

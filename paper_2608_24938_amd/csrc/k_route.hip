@@ -658,7 +658,9 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     int bm0, int bm1, int32_t *__restrict__ offsets, int32_t *__restrict__ tile_start0,
     int32_t *__restrict__ tile_start1, int32_t *__restrict__ row_token,
     int32_t *__restrict__ row_slot, float *__restrict__ row_w, int32_t *__restrict__ slot_row,
-    const int32_t *__restrict__ static_tgt, const float *__restrict__ static_scl, int identity) {
+    const int32_t *__restrict__ static_tgt, const float *__restrict__ static_scl, int identity,
+    const float *__restrict__ lpart, int lP, const float *__restrict__ bias,
+    float *__restrict__ logits_out, int32_t *__restrict__ ids_out, float *__restrict__ w_out) {
   __shared__ uint8_t sid[kDecodeFrontMaxSlots];   // expert of each slot (N <= 256)
   __shared__ float sw[kDecodeFrontMaxSlots];      // its weight
   __shared__ unsigned long long wsum[kMaxExperts];
@@ -716,9 +718,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   lds_barrier();
 
   // ---- pool (Eq. decode_budget): exact fixed-point weight sums ----
-  for (int j = tid; j < slots; j += kPoolThreads) {
-    const int e = clamp_id(ids[j], N);
-    const float wv = w[j];
+  auto add_slot = [&](int j, int e, float wv) {
     sid[j] = (uint8_t)e;
     sw[j] = wv;
     if (dynamic) {
@@ -726,6 +726,25 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
       atomicAdd(&wsum[e], (unsigned long long)q);
       atomicAdd(&cnt[e], 1);
     }
+  };
+  if (lpart) {
+    // Top-K and softmax of the batch here (small batches): wave w takes tokens
+    // w, w + kFrontWaves, ... with the per-token steps of route_tokens_kernel
+    for (int t = wave; t < B; t += kFrontWaves) {
+      float v[4];
+      wave_logit_row(lpart, lP, B, N, bias, t, lane, logits_out, v);
+      int my_id = 0;
+      float my_w = 0.f;
+      wave_topk_softmax(v, N, K, lane, my_id, my_w);
+      if (lane < K) {
+        const int j = t * K + lane;
+        ids_out[j] = my_id;
+        w_out[j] = my_w;
+        add_slot(j, my_id, my_w);
+      }
+    }
+  } else {
+    for (int j = tid; j < slots; j += kPoolThreads) add_slot(j, clamp_id(ids[j], N), w[j]);
   }
 #pragma unroll
   for (int b = 0; b < kFrontPfCols; ++b) {
@@ -896,13 +915,24 @@ hipError_t launch_decode_front(const int32_t *ids, const float *w, int B, int N,
                                const float *h, const float *S, const float *L, int32_t *pool,
                                int32_t *pool_size, int32_t *out_ids, float *out_w, int32_t *tgt,
                                float *scl, int t_shared, int bm0, int bm1, const PermBuffers &pb,
-                               const int32_t *static_tgt, const float *static_scl, hipStream_t s) {
+                               const int32_t *static_tgt, const float *static_scl, hipStream_t s,
+                               const FrontTopK &fused) {
   decode_front_kernel<<<1, kPoolThreads, 0, s>>>(ids, w, B, N, K, D, h, S, L, pool, pool_size, out_ids,
                                                  out_w, tgt, scl, t_shared, bm0, bm1, pb.offsets,
                                                  pb.tile_start0, pb.tile_start1, pb.row_token,
                                                  pb.row_slot, pb.row_w, pb.slot_row, static_tgt,
-                                                 static_scl, 0);
+                                                 static_scl, 0, fused.part, fused.P, fused.bias,
+                                                 fused.logits_out, fused.ids_out, fused.w_out);
   return hipGetLastError();
+}
+
+// One token per wave: with two, the second token's partial-logit loads wait
+// behind the first (32 tokens of the Mixtral-shaped layer: 16.7 us fused
+// against 5.2 + 8.4 us in two launches; one token of the Qwen3-shaped layer:
+// 12.5 us against 4.8 + 9.1 us).
+bool decode_front_fuses_topk(int B, int N) {
+  (void)N;
+  return B <= kFrontWaves;
 }
 
 hipError_t launch_permute_one_block(const int32_t *ids, const float *w, int T, int k_out, int N,
@@ -912,7 +942,8 @@ hipError_t launch_permute_one_block(const int32_t *ids, const float *w, int T, i
                                                  nullptr, nullptr, nullptr, nullptr, nullptr, nullptr,
                                                  t_shared, bm0, bm1, pb.offsets, pb.tile_start0,
                                                  pb.tile_start1, pb.row_token, pb.row_slot, pb.row_w,
-                                                 pb.slot_row, nullptr, nullptr, 1);
+                                                 pb.slot_row, nullptr, nullptr, 1, nullptr, 0,
+                                                 nullptr, nullptr, nullptr, nullptr);
   return hipGetLastError();
 }
 

@@ -51,11 +51,26 @@ hipError_t launch_permute(const int32_t *route_ids, const float *route_w, int T,
 // tables of a static pool) the pool and table steps are skipped; h, S, L,
 // pool, pool_size, tgt and scl are then unused.
 constexpr int kDecodeFrontMaxSlots = 8192;
+// With part != nullptr the front end also takes the per-token Top-K and softmax
+// from the P router partials (+ bias), writing ids_out/w_out [B, K] (and the
+// logits when logits_out is given); ids and w are then unused.  For batches
+// where decode_front_fuses_topk holds (at most one token per wave; one launch
+// fewer).
+struct FrontTopK {
+  const float *part = nullptr;
+  int P = 0;
+  const float *bias = nullptr;
+  float *logits_out = nullptr;
+  int32_t *ids_out = nullptr;
+  float *w_out = nullptr;
+};
+bool decode_front_fuses_topk(int B, int N);
 hipError_t launch_decode_front(const int32_t *ids, const float *w, int B, int N, int K, int D,
                                const float *h, const float *S, const float *L, int32_t *pool,
                                int32_t *pool_size, int32_t *out_ids, float *out_w, int32_t *tgt,
                                float *scl, int t_shared, int bm0, int bm1, const PermBuffers &pb,
-                               const int32_t *static_tgt, const float *static_scl, hipStream_t s);
+                               const int32_t *static_tgt, const float *static_scl, hipStream_t s,
+                               const FrontTopK &fused = FrontTopK{});
 // The stable permutation of launch_permute in one workgroup (the decode front
 // end with every expert mapped to itself), for T * k_out <= kDecodeFrontMaxSlots:
 // one launch instead of three.

@@ -58,6 +58,9 @@ def _forward_case(shape, T, phase, budget, seed=2):
     # 1024+ tokens: the router's many-token layout (32 tokens a workgroup for
     # 33-128 experts), with a ragged last workgroup
     (SHARED_BF16, 1100, "prefill", 2), (WIDE_BF16, 1500, "prefill", 4), (SMALL_BF16, 1030, "prefill", 1),
+    # small decode batches: Top-K and softmax inside the one-workgroup front end
+    (synth.TINY, 16, "decode", 4), (WIDE_BF16, 16, "decode", 16), (WIDE_F32, 20, "decode", 5),
+    (SHARED_BF16, 3, "decode", 8),
 ])
 def test_forward_matches_oracle(shape, T, phase, budget):
     lp, xs, (S, L, h), dbg, y = _forward_case(shape, T, phase, budget)
