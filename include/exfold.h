@@ -17,7 +17,8 @@
  * Memory.    Every tensor pointer is caller-owned DEVICE memory, contiguous and
  *            row-major, unless stated otherwise.  Outputs and workspaces are
  *            allocated by the caller; the library allocates no device memory
- *            and keeps no state besides a read-only cache of device properties.
+ *            and keeps no state besides a read-only cache of device properties
+ *            and the static scratch of exfold_moe_forward_scratch.
  *            The layer's weights and the token tensors x, y and x_cal are read
  *            and written in 16-byte vectors: their base pointers must be
  *            16-byte aligned (else EXFOLD_ERR_ALIGN).
@@ -63,7 +64,8 @@ enum {
   EXFOLD_ERR_DEVICE = 6,       /* a HIP launch or query failed                    */
   EXFOLD_ERR_UNSUPPORTED = 7,  /* valid request outside the kernels' limits       */
   EXFOLD_ERR_ARG = 8,          /* unknown phase or mode, or invalid scalar arg    */
-  EXFOLD_ERR_ALIGN = 9         /* a tensor pointer is not 16-byte aligned         */
+  EXFOLD_ERR_ALIGN = 9,        /* a tensor pointer is not 16-byte aligned         */
+  EXFOLD_ERR_SCRATCH = 10      /* needs more than EXFOLD_SCRATCH_BYTES of scratch */
 };
 
 enum { EXFOLD_F32 = 0, EXFOLD_BF16 = 1 };
@@ -266,6 +268,25 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
                                  const void *x, int64_t T, int32_t phase, int64_t budget,
                                  void *y, const exfold_debug *debug, void *ws, size_t ws_bytes,
                                  void *stream);
+
+/*
+ * exfold_moe_forward without a workspace, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops and harnesses
+ * that forbid hipMalloc).  The call allocates nothing: its intermediates live
+ * in a static scratch array of EXFOLD_SCRATCH_BYTES inside the library, one
+ * copy per GPU, held from the library's first use on that GPU until the
+ * process ends.  Arguments, outputs and errors are those of
+ * exfold_moe_forward (debug views included), plus EXFOLD_ERR_SCRATCH when
+ * exfold_moe_workspace_size(layer, T, phase, budget) > EXFOLD_SCRATCH_BYTES
+ * (returned before anything is enqueued).  Results are bit-identical to
+ * exfold_moe_forward's.  Every call on one GPU uses that GPU's single array,
+ * which keeps the last call's contents: calls that overlap on one GPU (other
+ * streams or host threads) race and must be serialised by the caller.
+ */
+#define EXFOLD_SCRATCH_BYTES ((size_t)64 << 20)
+exfold_status exfold_moe_forward_scratch(const exfold_layer *layer, const exfold_tables *tables,
+                                         const void *x, int64_t T, int32_t phase, int64_t budget,
+                                         void *y, const exfold_debug *debug, void *stream);
 
 /* Bytes of workspace exfold_moe_execute needs for T tokens of K_out routes. */
 size_t exfold_execute_workspace_size(const exfold_layer *layer, int64_t T, int64_t k_out);

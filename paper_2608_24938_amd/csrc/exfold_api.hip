@@ -325,6 +325,7 @@ const char *exfold_status_str(exfold_status s) {
     case EXFOLD_ERR_DEVICE: return "HIP launch failed";
     case EXFOLD_ERR_UNSUPPORTED: return "outside the kernels' limits";
     case EXFOLD_ERR_ARG: return "invalid phase, mode or scalar argument";
+    case EXFOLD_ERR_SCRATCH: return "request needs more than the static scratch (EXFOLD_SCRATCH_BYTES)";
     default: return "unknown status";
   }
 }
@@ -426,13 +427,13 @@ size_t exfold_moe_workspace_size(const exfold_layer *layer, int64_t T, int32_t p
   return p.total;
 }
 
-exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables *tables,
-                                 const void *x, int64_t T, int32_t phase, int64_t budget,
-                                 void *y, const exfold_debug *debug, void *ws, size_t ws_bytes,
-                                 void *stream) {
-  ForwardPlan p;
-  exfold_status st = plan_forward(layer, T, phase, budget, p);
-  if (st != EXFOLD_OK) return st;
+}  // extern "C"
+
+namespace {
+
+// Validation of a forward that needs no workspace (everything but the workspace checks).
+exfold_status check_forward(const exfold_layer *layer, const exfold_tables *tables, const void *x,
+                            int64_t T, int32_t phase, const void *y) {
   if (phase == EXFOLD_PHASE_DECODE_STATIC) {
     if (!tables || !tables->tgt || !tables->scl) return EXFOLD_ERR_NULL;
   } else if (phase == EXFOLD_PHASE_PREFILL_DIAG) {
@@ -445,9 +446,76 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
   if (T == 0) return EXFOLD_OK;
   if (!x || !y) return EXFOLD_ERR_NULL;
   if (misaligned(x) || misaligned(y)) return EXFOLD_ERR_ALIGN;
+  (void)layer;
+  return EXFOLD_OK;
+}
+
+exfold_status forward_impl(const exfold_layer *layer, const exfold_tables *tables, const void *x,
+                           const ForwardPlan &p, int32_t phase, void *y, const exfold_debug *debug,
+                           void *ws, hipStream_t s);
+
+// Scratch of exfold_moe_forward_scratch: one copy per GPU, held until the
+// process ends.  Host code never passes the array's name to a kernel (on the
+// host it is only a stand-in for the symbol); it uses the device address that
+// hipGetSymbolAddress returns for the current device.
+__device__ __align__(256) unsigned char scratch[EXFOLD_SCRATCH_BYTES];
+
+// Device address of `scratch` on the current device, queried once per device
+// with that device current; nullptr if the query fails.
+void *scratch_address() {
+  static std::mutex mu;
+  static void *cache[64] = {nullptr};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return nullptr;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!cache[dev]) {
+    void *ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr) return nullptr;
+    cache[dev] = ptr;
+  }
+  return cache[dev];
+}
+
+}  // namespace
+
+extern "C" {
+
+exfold_status exfold_moe_forward_scratch(const exfold_layer *layer, const exfold_tables *tables,
+                                         const void *x, int64_t T, int32_t phase, int64_t budget,
+                                         void *y, const exfold_debug *debug, void *stream) {
+  ForwardPlan p;
+  exfold_status st = plan_forward(layer, T, phase, budget, p);
+  if (st != EXFOLD_OK) return st;
+  st = check_forward(layer, tables, x, T, phase, y);
+  if (st != EXFOLD_OK || T == 0) return st;
+  if (p.total > EXFOLD_SCRATCH_BYTES) return EXFOLD_ERR_SCRATCH;
+  void *ws = scratch_address();
+  if (!ws) return EXFOLD_ERR_DEVICE;
+  return forward_impl(layer, tables, x, p, phase, y, debug, ws, static_cast<hipStream_t>(stream));
+}
+
+exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables *tables,
+                                 const void *x, int64_t T, int32_t phase, int64_t budget,
+                                 void *y, const exfold_debug *debug, void *ws, size_t ws_bytes,
+                                 void *stream) {
+  ForwardPlan p;
+  exfold_status st = plan_forward(layer, T, phase, budget, p);
+  if (st != EXFOLD_OK) return st;
+  st = check_forward(layer, tables, x, T, phase, y);
+  if (st != EXFOLD_OK || T == 0) return st;
   st = check_ws(ws, ws_bytes, p.total);
   if (st != EXFOLD_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
+  return forward_impl(layer, tables, x, p, phase, y, debug, ws, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"
+
+namespace {
+
+exfold_status forward_impl(const exfold_layer *layer, const exfold_tables *tables, const void *x,
+                           const ForwardPlan &p, int32_t phase, void *y, const exfold_debug *debug,
+                           void *ws, hipStream_t s) {
+  exfold_status st = EXFOLD_OK;
   const exfold_debug z{};
   const exfold_debug &dbg = debug ? *debug : z;
   float *part = at<float>(ws, p.o_logits);
@@ -527,6 +595,10 @@ exfold_status exfold_moe_forward(const exfold_layer *layer, const exfold_tables 
   record(dbg.events, EXFOLD_EV_END, s);
   return EXFOLD_OK;
 }
+
+}  // namespace
+
+extern "C" {
 
 size_t exfold_execute_workspace_size(const exfold_layer *layer, int64_t T, int64_t k_out) {
   ExecPlan p;

@@ -17,14 +17,17 @@ import torch
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libexfold.so")
 _lib = None
 
-OK, ERR_NULL, ERR_SHAPE, ERR_BUDGET, ERR_DTYPE, ERR_WORKSPACE, ERR_DEVICE, ERR_UNSUPPORTED, ERR_ARG, ERR_ALIGN = range(10)
+(OK, ERR_NULL, ERR_SHAPE, ERR_BUDGET, ERR_DTYPE, ERR_WORKSPACE, ERR_DEVICE, ERR_UNSUPPORTED, ERR_ARG, ERR_ALIGN,
+ ERR_SCRATCH) = range(11)
+SCRATCH_BYTES = 64 << 20   # EXFOLD_SCRATCH_BYTES
 F32, BF16 = 0, 1
 PHASE = {"dense": 0, "prefill": 1, "decode": 2, "decode_static": 3, "prefill_diag": 4}
 CAL_MODE = {"corouted": 0, "common": 1}
 
 EXPORTED = [
     "exfold_select_prefill", "exfold_select_decode_pool", "exfold_fold_gates", "exfold_static_pool",
-    "exfold_moe_workspace_size", "exfold_moe_forward", "exfold_execute_workspace_size",
+    "exfold_moe_workspace_size", "exfold_moe_forward", "exfold_moe_forward_scratch",
+    "exfold_execute_workspace_size",
     "exfold_moe_execute", "exfold_calibrate_workspace_size", "exfold_calibrate_projectors",
     "exfold_calibrate_diagonal",
     "exfold_status_str", "exfold_gemm_plan",
@@ -90,6 +93,7 @@ def lib() -> ctypes.CDLL:
             "exfold_static_pool": (i32, [vp, i64, i64, vp, vp, vp, vp, vp, vp, vp]),
             "exfold_moe_workspace_size": (sz, [vp, i64, i32, i64]),
             "exfold_moe_forward": (i32, [vp, vp, vp, i64, i32, i64, vp, vp, vp, sz, vp]),
+            "exfold_moe_forward_scratch": (i32, [vp, vp, vp, i64, i32, i64, vp, vp, vp]),
             "exfold_execute_workspace_size": (sz, [vp, i64, i64]),
             "exfold_moe_execute": (i32, [vp, vp, i64, i64, vp, vp, vp, vp, vp, sz, vp]),
             "exfold_calibrate_workspace_size": (sz, [vp, i64, i32]),
@@ -300,6 +304,30 @@ def moe_forward(layer: Layer, x, phase: str = "dense", budget: int = 0, S=None, 
     _check(lib().exfold_moe_forward(ctypes.byref(ls), None if tb is None else ctypes.byref(tb), _ptr(x), T,
                                     PHASE[phase], budget, _ptr(y), None if dbg is None else ctypes.byref(dbg),
                                     _ptr(workspace), workspace.numel(), _stream(stream)), "exfold_moe_forward")
+    return y
+
+
+def moe_forward_scratch(layer: Layer, x, phase: str = "dense", budget: int = 0, S=None, L=None, h=None, y=None,
+                        debug: dict | None = None, stream=None, static_tables=None,
+                        safeguards: dict | None = None, diag=None):
+    """moe_forward on the library's static scratch (exfold_moe_forward_scratch): no workspace is
+    allocated; y must be given by callers that cannot allocate (otherwise it is created here)."""
+    T = x.shape[0]
+    _need(x, layer.dtype, (T, layer.d), "x")
+    if y is None:
+        y = torch.empty_like(x)
+    ls = layer.struct()
+    tgt, scl = static_tables if static_tables is not None else (None, None)
+    cap, flags = fold_opts(**(safeguards or {}))
+    tb = _Tables(_ptr(S), _ptr(L), _ptr(h), _ptr(tgt), _ptr(scl), cap, flags, _ptr(diag)) \
+        if (S is not None or L is not None or tgt is not None) else None
+    dbg = None
+    if debug is not None:
+        dbg = _Debug(*[_ptr(debug.get(f)) for f in _DEBUG_FIELDS], None)
+    _check(lib().exfold_moe_forward_scratch(ctypes.byref(ls), None if tb is None else ctypes.byref(tb), _ptr(x), T,
+                                            PHASE[phase], budget, _ptr(y),
+                                            None if dbg is None else ctypes.byref(dbg), _stream(stream)),
+           "exfold_moe_forward_scratch")
     return y
 
 

@@ -32,7 +32,7 @@ def test_library_exports_every_declared_symbol():
 
 
 def test_status_strings():
-    for code in range(10):
+    for code in range(11):
         assert X.status_str(code)
     assert X.status_str(0) == "ok"
 
@@ -185,3 +185,25 @@ def test_execute_validation():
     assert L.exfold_moe_execute(ctypes.byref(ly), f, 64, 2, None, f, f, None, f * 16, n, None) == X.ERR_NULL
     assert L.exfold_moe_execute(ctypes.byref(ly), f + 8, 64, 2, f, f, f, None, f * 16, n, None) == X.ERR_ALIGN
     assert L.exfold_moe_execute(ctypes.byref(ly), f, 64, 2, f, f, f, None, f * 16, n - 1, None) == X.ERR_WORKSPACE
+
+
+def test_scratch_forward_validation():
+    # exfold_moe_forward_scratch: the forward's validation codes, then the scratch limit, all
+    # before any device call
+    L = X.lib()
+    ly = layer(dtype=X.BF16)
+    tb = X._Tables(FAKE, FAKE, FAKE, FAKE, FAKE, 0.0, 0, FAKE)
+    call = lambda T=64, phase=1, budget=1, tables=True, x=FAKE, y=FAKE: L.exfold_moe_forward_scratch(
+        ctypes.byref(ly), ctypes.byref(tb) if tables else None, x, T, phase, budget, y, None, None)
+    assert call(phase=5) == X.ERR_ARG
+    assert call(budget=0) == X.ERR_BUDGET
+    assert call(T=-1) == X.ERR_SHAPE
+    assert call(tables=False) == X.ERR_NULL
+    assert call(x=None) == X.ERR_NULL
+    assert call(y=FAKE + 2) == X.ERR_ALIGN
+    assert call(T=0) == X.OK
+    big = 1
+    while ws_size(ly, T=big, phase=2, budget=4) <= X.SCRATCH_BYTES:
+        big *= 2
+    assert call(T=big, phase=2, budget=4) == X.ERR_SCRATCH
+    assert X.status_str(X.ERR_SCRATCH).startswith("request needs more than the static scratch")
