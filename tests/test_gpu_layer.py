@@ -64,40 +64,72 @@ def _forward_case(shape, T, phase, budget, seed=2):
 ])
 def test_forward_matches_oracle(shape, T, phase, budget):
     lp, xs, (S, L, h), dbg, y = _forward_case(shape, T, phase, budget)
+    N, K = shape.n_experts, shape.top_k
     x = synth.widen(xs)
+    g = {k: v.cpu().numpy() for k, v in dbg.items()}
     # router logits within the float32 rounding bound
     ref_logits = O.router_logits(x, lp.ref.w_router, lp.ref.router_bias)
     bound = logits_bound(x, lp.ref.w_router, lp.ref.router_bias, shape.d)
-    g_logits = dbg["logits"].cpu().numpy().astype(np.float64)
-    assert np.all(np.abs(g_logits - ref_logits) <= bound)
-    # oracle forward from x (its own float64 routing)
-    y_ref, info = O.moe_forward(lp.ref, x, shape.top_k, phase, budget, S, L, h)
-    tie = topk_near_tie(ref_logits, bound, shape.top_k)
-    g_ids = dbg["topk_ids"].cpu().numpy()
-    same_routes = np.all(g_ids == info["topk_ids"], axis=1)
-    assert np.all(same_routes | tie), "route mismatch away from a near-tie"
-    ok = same_routes.copy()
+    assert np.all(np.abs(g["logits"].astype(np.float64) - ref_logits) <= bound)
+
+    # stage by stage from the device's own logits and routes: discrete results bit-exact
+    ids, w = g["topk_ids"], g["topk_w"]
+    r_ids, r_w = O.route(g["logits"], K)
+    np.testing.assert_array_equal(ids, r_ids)
+    np.testing.assert_allclose(w, r_w, rtol=2 ** -22, atol=0)
     if phase == "prefill":
-        same_fold = np.all(dbg["fold_ids"].cpu().numpy() == info["fold_ids"], axis=1)
-        ok &= same_fold
-        assert same_fold[same_routes].mean() >= 0.99
+        keep = O.select_prefill(ids, w, h, budget)
+        np.testing.assert_array_equal(g["keep"].astype(bool), keep)
+        f_ids, f_w = O.fold_prefill(ids, w, keep, S, L)
     elif phase == "decode":
-        n = int(dbg["pool_size"].item())
-        assert n == len(info["pool"])
-        g_pool = dbg["pool"].cpu().numpy()[:n].tolist()
+        pool, _ = O.select_decode_pool(ids, w, h, N, budget)
+        n = int(g["pool_size"][0])
+        assert g["pool"][:n].tolist() == pool
+        f_ids, f_w, _, _ = O.fold_decode(ids, w, pool, S, L, N)
+    else:
+        f_ids, f_w = ids, w
+    ex_ids = g["fold_ids"] if phase != "dense" else ids
+    ex_w = g["fold_w"] if phase != "dense" else w
+    np.testing.assert_array_equal(ex_ids, f_ids)
+    np.testing.assert_array_equal(ex_w.view(np.uint32), f_w.view(np.uint32))
+
+    # end to end from x: the oracle's own float64 routing, selection and fold
+    y_ref, info = O.moe_forward(lp.ref, x, K, phase, budget, S, L, h)
+    tie = topk_near_tie(ref_logits, bound, K)
+    same_routes = np.all(ids == info["topk_ids"], axis=1)
+    assert np.all(same_routes | tie), "route mismatch away from a near-tie"
+    same_exec = np.all(ex_ids == info["fold_ids"], axis=1)
+    allowed = max(2, T // 50)
+    if phase == "prefill":
+        # equal routes, different selection: only where the oracle's scores w*h tie within
+        # the one-ulp difference of the two softmax weights
+        for i in np.nonzero(same_routes & ~same_exec)[0]:
+            sc = np.sort(info["topk_w"][i].astype(np.float64) * h[info["topk_ids"][i]].astype(np.float64))[::-1]
+            kp = min(budget, K)
+            assert sc[kp - 1] - sc[kp] <= 1e-5 * sc[0], ("selection differs away from a near-tie", i)
+    elif phase == "decode":
+        g_pool = g["pool"][: int(g["pool_size"][0])].tolist()
+        assert len(g_pool) == len(info["pool"])
         if g_pool != info["pool"]:
-            # only a near-tie of the batch scores may reorder the pool: check the margin
-            w = info["topk_w"].astype(np.float64)
-            score = np.zeros(shape.n_experts)
-            np.add.at(score, info["topk_ids"].reshape(-1), w.reshape(-1))
+            # only a near-tie of the batch scores may change the pool: check the margin
+            wr = info["topk_w"].astype(np.float64)
+            score = np.zeros(N)
+            np.add.at(score, info["topk_ids"].reshape(-1), wr.reshape(-1))
             score *= h.astype(np.float64)
             diff = sorted(set(g_pool) ^ set(info["pool"]))
             assert np.ptp(score[diff]) <= 1e-5 * score.max(), "pool differs away from a near-tie"
-            ok &= ~np.isin(info["topk_ids"], diff).any(axis=1)
-        np.testing.assert_array_equal(dbg["fold_ids"].cpu().numpy()[ok], info["fold_ids"][ok])
-    assert ok.mean() >= 0.9, ok.mean()
-    err = per_token_rel_l2(y, y_ref)[ok]
-    assert err.max() <= TOL_Y[shape.dtype], err.max()
+            allowed = T      # a changed pool moves every token routed to the experts that changed
+    # every token's y: against the oracle's own output where the executed routes agree, and
+    # against the oracle on the device's executed routes where a near-tie changed them
+    y_cmp = y_ref.copy()
+    moved = np.nonzero(~same_exec)[0]
+    if moved.size:
+        y_cmp[moved] = O.moe_output(lp.ref, x[moved], ex_ids[moved], ex_w[moved])
+    err = per_token_rel_l2(y, y_cmp)
+    assert err.max() <= TOL_Y[shape.dtype], (err.max(), int(np.argmax(err)))
+    assert moved.size <= allowed, f"{moved.size} of {T} tokens left the oracle's routes"
+    print(f"{shape.name} {phase} T={T}: max rel-L2 {err.max():.2e}, tokens on other routes {moved.size}",
+          flush=True)
 
 
 @pytest.mark.parametrize("shape,T,K_id,D_id", [(WIDE_F32, 64, 8, 64), (WIDE_BF16, 200, 8, 128),
@@ -197,7 +229,7 @@ def test_calibration_matches_oracle(shape, m, mode, lam, clip):
     rS, rL, rh, rst = O.calibrate(lp.ref, synth.widen(xs), shape.top_k, lam=lam, clip=clip, mode=mode)
     st = st.cpu().numpy()
     np.testing.assert_array_equal(st[..., 3], rst["n"])
-    tol = 1e-4 if shape.dtype == "f32" else 2e-2
+    tol = 1e-4 if shape.dtype == "f32" else 1e-2
     obs = rst["n"] > 0
     np.testing.assert_allclose(st[..., 0][obs], rst["A"][obs], rtol=tol, atol=tol * np.abs(rst["A"]).max())
     np.testing.assert_allclose(st[..., 1][obs], rst["V"][obs], rtol=tol)
