@@ -625,7 +625,7 @@ def calibrate(layer: Layer, x_cal, top_k: int, lam: float = DEFAULT_LAMBDA,
 
 
 # ---------------------------------------------------------------------------
-# Diagonal projector family  (Appendix A, Eq. appendix_diagonal_projector; the
+# Diagonal projector family  (Appendix B, Eq. appendix_diagonal_projector; the
 # unfused reconstruction path of the projector ablation)
 # ---------------------------------------------------------------------------
 

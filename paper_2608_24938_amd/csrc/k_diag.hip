@@ -1,4 +1,4 @@
-// Diagonal projector family (Appendix A, Eq. appendix_diagonal_projector): the
+// Diagonal projector family (Appendix B, Eq. appendix_diagonal_projector): the
 // unfused reconstruction path of the projector ablation.
 //
 // stats:   per ordered pair (s, t), in token order over the calibration tokens

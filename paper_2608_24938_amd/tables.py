@@ -1,7 +1,7 @@
 """Persistence of calibrated projector tables.
 
 The projector tables are computed once per model on calibration tokens and then
-kept fixed (Sec. 3.2; the calibrated state is two N x N float32 tables per MoE
+kept fixed (Sec. 4.2; the calibrated state is two N x N float32 tables per MoE
 layer, Table 3's storage arithmetic, plus the per-expert output norms h).  This
 module writes and reads them as one little-endian file:
 
@@ -26,7 +26,8 @@ import numpy as np
 MAGIC = b"EXFT"
 VERSION = 1
 _HEADER = struct.Struct("<4sIIIffIII")
-MODES = {"corouted": 0, "common_input": 1}
+MODES = {"corouted": 0, "common": 1}          # the binding's calibration mode names
+_ALIASES = {"common_input": "common", "co-routed": "corouted"}
 
 
 @dataclass
@@ -57,6 +58,7 @@ def save_tables(path: str, layers, lam: float = 1e-3, clip: float = 4.0, mode: s
     n = _host(rows[0].S).shape[0]
     diag = rows[0].Dg is not None
     d = _host(rows[0].Dg).shape[2] if diag else 0
+    mode = _ALIASES.get(mode, mode)
     if mode not in MODES:
         raise ValueError(f"unknown calibration mode {mode!r}")
     with open(path, "wb") as f:

@@ -1,4 +1,4 @@
-"""Diagonal projectors on the GPU (Appendix A, Eq. appendix_diagonal_projector;
+"""Diagonal projectors on the GPU (Appendix B, Eq. appendix_diagonal_projector;
 the unfused reconstruction path): calibration of the per-dimension maps and
 their loss, and the prefill forward that applies them element-wise."""
 

@@ -25,10 +25,10 @@ def _layers(n_layers, n, d=0, seed=0):
 def test_round_trip_is_bitwise(tmp_path, d):
     layers = _layers(3, 8, d)
     path = tmp_path / "t.bin"
-    nbytes = save_tables(str(path), layers, lam=1e-3, clip=4.0, mode="common_input")
+    nbytes = save_tables(str(path), layers, lam=1e-3, clip=4.0, mode="common")
     assert path.stat().st_size == nbytes
     back, meta = load_tables(str(path))
-    assert meta == {"lambda": np.float32(1e-3), "clip": 4.0, "mode": "common_input", "n_experts": 8, "d": d}
+    assert meta == {"lambda": np.float32(1e-3), "clip": 4.0, "mode": "common", "n_experts": 8, "d": d}
     for a, b in zip(layers, back):
         for f in ("S", "L", "h"):
             np.testing.assert_array_equal(getattr(a, f).view(np.uint32), getattr(b, f).view(np.uint32))
@@ -84,3 +84,37 @@ def test_inconsistent_layers_are_rejected(tmp_path):
         save_tables(str(tmp_path / "t.bin"), [a, b])
     with pytest.raises(ValueError):
         save_tables(str(tmp_path / "t.bin"), [a], mode="other")
+
+
+def test_mode_names_are_the_bindings(tmp_path):
+    # the calibration mode strings of exfold.calibrate_projectors are accepted as they are
+    from paper_2608_24938_amd import exfold as X
+    for mode in X.CAL_MODE:
+        save_tables(str(tmp_path / "m.bin"), _layers(1, 4), mode=mode)
+        assert load_tables(str(tmp_path / "m.bin"))[1]["mode"] == mode
+    save_tables(str(tmp_path / "m.bin"), _layers(1, 4), mode="common_input")
+    assert load_tables(str(tmp_path / "m.bin"))[1]["mode"] == "common"
+
+
+@pytest.mark.gpu
+def test_calibrate_save_load_forward(tmp_path):
+    """Tables calibrated on the device, written, read back and used: the forward with the loaded
+    tables is bit-identical to the forward with the tables as calibrated."""
+    import torch
+    from paper_2608_24938_amd import exfold as X
+
+    from .gpu_common import LayerPair, sync, to_dev
+    shape = synth.LayerShape("tables-bf16", d=256, inter=128, n_experts=32, top_k=4, dtype="bf16")
+    lp = LayerPair(shape, seed=3)
+    for mode in X.CAL_MODE:
+        S, L, h = X.calibrate_projectors(lp.dev, to_dev(synth.calibration_tokens(shape, 512, 3)), mode=mode)
+        path = tmp_path / f"{mode}.bin"
+        save_tables(str(path), [(S, L, h)], mode=mode)
+        (t,), meta = load_tables(str(path))
+        assert meta["mode"] == mode
+        x = to_dev(synth.tokens(shape, 200, 3))
+        for phase, budget in (("prefill", 2), ("decode", 8)):
+            y0 = X.moe_forward(lp.dev, x, phase, budget, S, L, h)
+            y1 = X.moe_forward(lp.dev, x, phase, budget, to_dev(t.S), to_dev(t.L), to_dev(t.h))
+            sync()
+            assert torch.equal(y0.view(torch.int16), y1.view(torch.int16)), (mode, phase)
