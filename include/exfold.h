@@ -78,7 +78,7 @@ enum {
                                      (Appendix B, Eq. appendix_decode_static_budget,
                                      Eq. appendix_decode_remap); see exfold_static_pool */
   EXFOLD_PHASE_PREFILL_DIAG = 4   /* per-token K' budget with diagonal projectors on the
-                                     unfused path (Appendix A,
+                                     unfused path (Appendix B,
                                      Eq. appendix_diagonal_projector); see
                                      exfold_calibrate_diagonal */
 };
@@ -357,7 +357,7 @@ exfold_status exfold_gemm_plan(const exfold_layer *layer, int64_t rows, int64_t 
                                int32_t cu_count, int32_t *out);
 
 /*
- * Diagonal projector calibration (Appendix A, Eq. appendix_diagonal_projector;
+ * Diagonal projector calibration (Appendix B, Eq. appendix_diagonal_projector;
  * the unfused family of the projector ablation).  Routing, evaluated pairs and
  * the weight w = ||u||_2 are those of exfold_calibrate_projectors.  Per ordered
  * pair (s, t), in token order and float64, per hidden dimension n:

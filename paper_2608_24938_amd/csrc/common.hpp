@@ -83,6 +83,14 @@ __device__ __forceinline__ uint64_t wave_reduce_u64(uint64_t v) {
   return pick(pick(readlane_u64(v, 0), readlane_u64(v, 16)), pick(readlane_u64(v, 32), readlane_u64(v, 48)));
 }
 __device__ __forceinline__ uint64_t wave_max_u64(uint64_t v) { return wave_reduce_u64<true>(v); }
+// Max of a 32-bit value over the wave; every lane gets the result.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, dpp_u32<0xB1>(v, v));
+  v = max(v, dpp_u32<0x4E>(v, v));
+  v = max(v, dpp_u32<0x141>(v, v));
+  v = max(v, dpp_u32<0x140>(v, v));
+  return max(max(readlane_u32(v, 0), readlane_u32(v, 16)), max(readlane_u32(v, 32), readlane_u32(v, 48)));
+}
 __device__ __forceinline__ uint64_t wave_min_u64(uint64_t v) { return wave_reduce_u64<false>(v); }
 
 // Sum over the wave in a fixed association (pairs within quads, half-rows,

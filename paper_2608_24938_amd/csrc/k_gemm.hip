@@ -1248,40 +1248,76 @@ __device__ __forceinline__ float4 load4<bf16_t>(const bf16_t *p) {
                      __uint_as_float(u.y << 16), __uint_as_float(u.y & 0xffff0000u));
 }
 
-template <typename InT, typename OutT>
+template <typename InT, int C>
+__device__ __forceinline__ void load_cols(const InT *p, float (&v)[C]) {
+#pragma unroll
+  for (int q = 0; q < C; q += 4) {
+    const float4 f = load4<InT>(p + q);
+    v[q] = f.x;
+    v[q + 1] = f.y;
+    v[q + 2] = f.z;
+    v[q + 3] = f.w;
+  }
+}
+
+template <typename InT, typename OutT, int C>
 __global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y, int ksplit,
                                                      int rows, const int32_t *__restrict__ slot_row,
                                                      int k_out, int d, int shared_base,
                                                      OutT *__restrict__ y) {
-  // block (i, c): token i, columns [2048 c, 2048 c + 2048), eight per thread
-  // (16-byte loads of bf16 rows and 16-byte bf16 stores)
+  // block (i, c): token i, columns [256 C c, 256 C (c + 1)), C per thread.  The
+  // token's row indices are loaded first (one round trip), then the rows are
+  // loaded four at a time and added in slot order, split partials in order.
   const int i = blockIdx.x;
-  const int c = blockIdx.y * 2048 + threadIdx.x * 8;
+  const int c = (blockIdx.y * 256 + threadIdx.x) * C;
   if (c >= d) return;
   const long long split = (long long)rows * d;
-  float acc[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
-  for (int k = 0; k <= k_out; ++k) {
-    long long r;
-    if (k < k_out)
-      r = slot_row[(long long)i * k_out + k];
-    else if (shared_base >= 0)
-      r = shared_base + i;
-    else
-      break;
-    for (int sp = 0; sp < ksplit; ++sp) {
-      const InT *src = Y + sp * split + r * d + c;
-      const float4 v0 = load4<InT>(src), v1 = load4<InT>(src + 4);
-      acc[0] += v0.x; acc[1] += v0.y; acc[2] += v0.z; acc[3] += v0.w;
-      acc[4] += v1.x; acc[5] += v1.y; acc[6] += v1.z; acc[7] += v1.w;
+  const int nr = k_out + (shared_base >= 0 ? 1 : 0);
+  int r[kMaxTopK + 1];
+#pragma unroll
+  for (int k = 0; k <= kMaxTopK; ++k)
+    r[k] = (k < k_out) ? slot_row[(long long)i * k_out + k] : (k == k_out && shared_base >= 0) ? shared_base + i : 0;
+  float acc[C];
+#pragma unroll
+  for (int q = 0; q < C; ++q) acc[q] = 0.f;
+  for (int sp = 0; sp < ksplit; ++sp) {
+    // split sp of every row; with one split this is the whole sum in slot order
+    const InT *base = Y + sp * split + c;
+#pragma unroll
+    for (int k0 = 0; k0 <= kMaxTopK; k0 += 4) {
+      if (k0 >= nr) break;
+      float v[4][C];
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (k0 + u < nr) load_cols<InT, C>(base + (long long)r[k0 + u] * d, v[u]);
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+        if (k0 + u < nr) {
+#pragma unroll
+          for (int q = 0; q < C; ++q) acc[q] += v[u][q];
+        }
     }
   }
   OutT *o = y + (long long)i * d + c;
-  if constexpr (sizeof(OutT) == 2) {
-    store4_bf16(reinterpret_cast<bf16_t *>(o), acc[0], acc[1], acc[2], acc[3]);
-    store4_bf16(reinterpret_cast<bf16_t *>(o) + 4, acc[4], acc[5], acc[6], acc[7]);
+#pragma unroll
+  for (int q = 0; q < C; q += 4) {
+    if constexpr (sizeof(OutT) == 2)
+      store4_bf16(reinterpret_cast<bf16_t *>(o) + q, acc[q], acc[q + 1], acc[q + 2], acc[q + 3]);
+    else
+      *reinterpret_cast<float4 *>(o + q) = make_float4(acc[q], acc[q + 1], acc[q + 2], acc[q + 3]);
+  }
+}
+
+template <typename InT, typename OutT>
+static void launch_combine_t(const InT *Y, int ksplit, int rows, const int32_t *slot_row, int T, int k_out,
+                             int d, int shared_base, OutT *y, hipStream_t s) {
+  // eight columns a thread once the grid covers the CUs a few times over; four below
+  if ((long long)T * d >= 256LL * 256 * 8 * 4) {
+    const dim3 grid(T, (d + 2047) / 2048);
+    combine_kernel<InT, OutT, 8><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
   } else {
-    *reinterpret_cast<float4 *>(o) = make_float4(acc[0], acc[1], acc[2], acc[3]);
-    *reinterpret_cast<float4 *>(o + 4) = make_float4(acc[4], acc[5], acc[6], acc[7]);
+    const dim3 grid(T, (d + 1023) / 1024);
+    combine_kernel<InT, OutT, 4><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
   }
 }
 
@@ -1289,17 +1325,14 @@ hipError_t launch_combine(int dtype, const float *Y, bool y_bf16, int ksplit, in
                           const int32_t *slot_row, int T, int k_out, int d, int shared_base, void *y,
                           hipStream_t s) {
   if (T <= 0) return hipSuccess;
-  const dim3 grid(T, (d + 2047) / 2048);
   if (dtype == EXFOLD_BF16 && y_bf16)
-    combine_kernel<bf16_t, bf16_t><<<grid, 256, 0, s>>>(reinterpret_cast<const bf16_t *>(Y), ksplit,
-                                                        rows, slot_row, k_out, d, shared_base,
-                                                        static_cast<bf16_t *>(y));
+    launch_combine_t<bf16_t, bf16_t>(reinterpret_cast<const bf16_t *>(Y), ksplit, rows, slot_row, T, k_out, d,
+                                     shared_base, static_cast<bf16_t *>(y), s);
   else if (dtype == EXFOLD_BF16)
-    combine_kernel<float, bf16_t><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
-                                                       static_cast<bf16_t *>(y));
+    launch_combine_t<float, bf16_t>(Y, ksplit, rows, slot_row, T, k_out, d, shared_base,
+                                    static_cast<bf16_t *>(y), s);
   else
-    combine_kernel<float, float><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base,
-                                                      static_cast<float *>(y));
+    launch_combine_t<float, float>(Y, ksplit, rows, slot_row, T, k_out, d, shared_base, static_cast<float *>(y), s);
   return hipGetLastError();
 }
 

@@ -110,6 +110,110 @@ __global__ __launch_bounds__(64 * KS) void router_logits_bf16(const bf16_t *__re
   }
 }
 
+// Many tokens and many experts: 32 tokens per workgroup, one wave per 16
+// experts owning its experts over the whole of d (no cross-wave reduction).
+// The tokens' x rows pass through LDS in chunks of 256 along d (double
+// buffered, loaded one chunk ahead through registers); each wave streams its
+// W_r rows from global (L2-resident), the next chunk's fragments in flight
+// during the current chunk's MFMAs.  One pass writes the logits (P = 1).
+constexpr int kRlTok = 32, kRlChunk = 256, kRlPad = 8;
+constexpr int kRlRow = kRlChunk + kRlPad;  // LDS row stride (bf16): 16 rows of one read spread over the banks
+
+template <int NW>
+__global__ __launch_bounds__(64 * NW) void router_logits_lds(const bf16_t *__restrict__ x,
+                                                            const bf16_t *__restrict__ wr, int T, int N,
+                                                            int d, float *__restrict__ out) {
+  __shared__ __attribute__((aligned(16))) bf16_t xs[2][kRlTok * kRlRow];
+  constexpr int kThreads = 64 * NW;
+  constexpr int kChunks16 = kRlTok * kRlChunk / 8;           // 16-byte pieces of one x chunk
+  constexpr int kPer = (kChunks16 + kThreads - 1) / kThreads;  // per thread
+  const int tid = threadIdx.x, wave = tid >> 6, lane = tid & 63;
+  const int t0 = blockIdx.x * kRlTok;
+  const int e = wave * 16 + (lane & 15);
+  const bool live = e < N;
+  const bf16_t *wrow = wr + (size_t)(live ? e : 0) * d + (lane >> 4) * 8;
+  const int nch = d / kRlChunk;
+
+  u32x4 xr[kPer];
+  auto load_x = [&](int ch) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = i * kThreads + tid;
+      if (c < kChunks16) {
+        const int r = c / (kRlChunk / 8), q = c % (kRlChunk / 8);
+        const int t = min(t0 + r, T - 1);
+        xr[i] = *reinterpret_cast<const u32x4 *>(x + (size_t)t * d + ch * kRlChunk + q * 8);
+      }
+    }
+  };
+  auto store_x = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int c = i * kThreads + tid;
+      if (c < kChunks16) {
+        const int r = c / (kRlChunk / 8), q = c % (kRlChunk / 8);
+        *reinterpret_cast<u32x4 *>(&xs[buf][r * kRlRow + q * 8]) = xr[i];
+      }
+    }
+  };
+  constexpr int kSteps = kRlChunk / 32;
+  auto load_w = [&](int ch, bf16x8 (&dst)[kSteps]) {
+#pragma unroll
+    for (int k = 0; k < kSteps; ++k)
+      dst[k] = *reinterpret_cast<const bf16x8 *>(wrow + ch * kRlChunk + k * 32);
+  };
+  f32x4 acc[2] = {f32x4{0.f, 0.f, 0.f, 0.f}, f32x4{0.f, 0.f, 0.f, 0.f}};
+  bf16x8 zero;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) zero[q] = (__bf16)0.0f;
+  auto compute = [&](int buf, const bf16x8 (&wb)[kSteps]) {
+    const bf16_t *xa = &xs[buf][(lane & 15) * kRlRow + (lane >> 4) * 8];
+#pragma unroll
+    for (int k = 0; k < kSteps; ++k) {
+      const bf16x8 b = live ? wb[k] : zero;
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const bf16x8 a = *reinterpret_cast<const bf16x8 *>(xa + u * 16 * kRlRow + k * 32);
+        acc[u] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[u], 0, 0, 0);
+      }
+    }
+  };
+  // chunk ch: its W_r fragments were loaded one chunk ahead (wb0 for even
+  // chunks, wb1 for odd), its x rows stored to LDS buffer ch & 1 before the
+  // barrier that ends chunk ch - 1
+  bf16x8 wb0[kSteps], wb1[kSteps];
+  load_x(0);
+  load_w(0, wb0);
+  store_x(0);
+  if (nch > 1) load_x(1);
+  __syncthreads();
+  for (int ch = 0; ch < nch; ch += 2) {
+    if (ch + 1 < nch) load_w(ch + 1, wb1);
+    compute(0, wb0);
+    if (ch + 1 < nch) {
+      store_x(1);
+      if (ch + 2 < nch) load_x(ch + 2);
+    }
+    __syncthreads();
+    if (ch + 1 >= nch) break;
+    if (ch + 2 < nch) load_w(ch + 2, wb0);
+    compute(1, wb1);
+    if (ch + 2 < nch) {
+      store_x(0);
+      if (ch + 3 < nch) load_x(ch + 3);
+    }
+    __syncthreads();
+  }
+  // acc[u][i]: token t0 + 16 u + 4 (lane / 16) + i, expert e
+#pragma unroll
+  for (int u = 0; u < 2; ++u)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int t = t0 + u * 16 + (lane >> 4) * 4 + i;
+      if (t < T && live) out[(size_t)t * N + e] = acc[u][i];
+    }
+}
+
 // Blocks of the all-experts layout at or above which the d axis is not split.
 constexpr int kRouterWideBlocks = 64;
 
@@ -165,6 +269,12 @@ hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, 
       // 16 tokens x 16 experts x d/P per block
       const dim3 grid(tb, (N + 15) / 16, P);
       router_logits_bf16<1, 4><<<grid, 256, 0, s>>>(xb, wb, T, N, d, d / P, part);
+    } else if (N > 32 && d % kRlChunk == 0) {
+      // one wave per 16 experts over the whole of d
+      const int nt = (N + 15) / 16, grid = (T + kRlTok - 1) / kRlTok;
+      if (nt <= 4) router_logits_lds<4><<<grid, 256, 0, s>>>(xb, wb, T, N, d, part);
+      else if (nt <= 8) router_logits_lds<8><<<grid, 512, 0, s>>>(xb, wb, T, N, d, part);
+      else router_logits_lds<16><<<grid, 1024, 0, s>>>(xb, wb, T, N, d, part);
     } else {
       const int nt = (N + 15) / 16;
       if (nt <= 1) launch_router_wide<1>(xb, wb, T, N, d, part, s);
@@ -219,23 +329,29 @@ __device__ __forceinline__ void wave_logit_row(const float *__restrict__ part, i
 // float64 and rounded once to float32.
 __device__ __forceinline__ void wave_topk_softmax(const float v[4], int N, int K, int lane,
                                                   int &my_id, float &my_w) {
-  uint64_t key[4];
+  // 32-bit order keys (0 marks a taken or absent expert); each round takes the
+  // wave maximum with DPP, then the smallest expert id holding it from ballots
+  // (ids lane + 64 j grow with j, then with the lane)
+  uint32_t key[4];
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    const int e = lane + 64 * j;
-    key[j] = (e < N) ? ((uint64_t(float_key(v[j])) << 32) | uint64_t(0xffffffffu - uint32_t(e))) : 0ull;
-  }
+  for (int j = 0; j < 4; ++j) key[j] = (lane + 64 * j < N) ? float_key(v[j]) : 0u;
   my_id = 0;
   for (int k = 0; k < K; ++k) {
-    uint64_t best = key[0];
+    const uint32_t best = wave_max_u32(max(max(key[0], key[1]), max(key[2], key[3])));
+    int id = 0;
+    bool found = false;
 #pragma unroll
-    for (int j = 1; j < 4; ++j) best = key[j] > best ? key[j] : best;
-    best = wave_max_u64(best);
-    const int id = int(0xffffffffu - uint32_t(best & 0xffffffffu));
+    for (int j = 0; j < 4; ++j) {
+      const uint64_t m = __ballot(key[j] == best);
+      if (!found && m != 0ull) {
+        id = 64 * j + (int)__builtin_ctzll(m);
+        found = true;
+      }
+    }
     if (lane == k) my_id = id;
 #pragma unroll
     for (int j = 0; j < 4; ++j)
-      if (lane + 64 * j == id) key[j] = 0ull;
+      if (lane + 64 * j == id) key[j] = 0u;
   }
   my_id = clamp_id(my_id, N);
   // logit of my route: held by lane my_id % 64 in register my_id / 64
@@ -260,6 +376,13 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   const int lane = threadIdx.x & 63;
   const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
   if (t >= T) return;  // uniform per wave
+  // h of experts lane + 64 j, loaded with the logits (no load after Top-K)
+  float hv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (h && !keep_in) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (lane + 64 * j < N) hv[j] = h[lane + 64 * j];
+  }
   int my_id = 0;
   float my_w = 0.f;
   if (part) {
@@ -281,7 +404,12 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   if (keep_in) {
     kept = (lane < K) && keep_in[(size_t)t * K + lane] != 0;
   } else {
-    const double score = (lane < K) ? (double)my_w * (double)h[my_id] : 0.0;
+    // h of my route: held by lane my_id % 64 in register my_id / 64
+    const int hs = my_id & 63, hr = my_id >> 6;
+    const float h0 = __shfl(hv[0], hs, kWave), h1 = __shfl(hv[1], hs, kWave);
+    const float h2 = __shfl(hv[2], hs, kWave), h3 = __shfl(hv[3], hs, kWave);
+    const float h_my = hr == 0 ? h0 : hr == 1 ? h1 : hr == 2 ? h2 : h3;
+    const double score = (lane < K) ? (double)my_w * (double)h_my : 0.0;
     int rank = 0;
     for (int j = 0; j < K; ++j) {
       const double sj = readlane_f64(score, j);
@@ -306,16 +434,23 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   int tgt_lane = -1;
   double contrib = 0.0, rest = 0.0;
   if (lane < K && !kept) {
+    // L and S of every candidate target loaded together (one round trip)
     const float *lrow = L + (size_t)my_id * N;
-    float lv[kMaxTopK];
+    const float *srow = S ? S + (size_t)my_id * N : nullptr;
+    float lv[kMaxTopK], sv[kMaxTopK];
 #pragma unroll
-    for (int j = 0; j < kMaxTopK; ++j) lv[j] = (j < K && ((kmask >> j) & 1ull)) ? lrow[ids[j]] : 0.f;
-    float best = 0.f;
+    for (int j = 0; j < kMaxTopK; ++j) {
+      const bool cand = j < K && ((kmask >> j) & 1ull);
+      lv[j] = cand ? lrow[ids[j]] : 0.f;
+      sv[j] = (cand && srow && !om_src) ? srow[ids[j]] : 0.f;
+    }
+    float best = 0.f, s_best = 0.f;
 #pragma unroll
     for (int j = 0; j < kMaxTopK; ++j) {
       if (j < K && ((kmask >> j) & 1ull) && (!capped || lv[j] <= loss_cap)) {
         if (tgt_lane < 0 || lv[j] < best) {
           best = lv[j];
+          s_best = sv[j];
           tgt_lane = j;
         }
       }
@@ -323,7 +458,7 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
     if (tgt_lane >= 0 && !om_src) {
       double c = 1.0;
       if (conf) c = fmin(1.0, fmax(0.0, __dsub_rn(1.0, (double)best)));
-      contrib = __dmul_rn(__dmul_rn((double)my_w, c), (double)S[(size_t)my_id * N + ids[tgt_lane]]);
+      contrib = __dmul_rn(__dmul_rn((double)my_w, c), (double)s_best);
       if (conf) rest = __dmul_rn((double)my_w, __dsub_rn(1.0, c));
     }
   }
@@ -507,10 +642,13 @@ __global__ __launch_bounds__(kPoolThreads) void decode_pool_fold_kernel(
 // atomic min per source combines the threads, and the one thread whose key won
 // writes the target and its scale.  Called by the whole workgroup (it holds
 // two barriers); pool/in_pool/n_pool in LDS; writes tgt/scl (LDS) and
-// tgt_g/scl_g (either may be NULL).
+// tgt_g/scl_g (either may be NULL).  need (LDS, or NULL for every source):
+// only sources with need[s] > 0 get tables (the routed ones, when no table
+// output is asked for: no other entry is read).
 __device__ void pool_tables(int N, const float *__restrict__ S, const float *__restrict__ L,
                             const int *pool, const int *in_pool, int n_pool, int *tgt, float *scl,
-                            int32_t *__restrict__ tgt_g, float *__restrict__ scl_g) {
+                            int32_t *__restrict__ tgt_g, float *__restrict__ scl_g,
+                            const int *need = nullptr) {
   constexpr int kBatch = 8;  // loads in flight per thread
   __shared__ unsigned long long best[kMaxExperts];
   const int tid = threadIdx.x;
@@ -518,7 +656,7 @@ __device__ void pool_tables(int N, const float *__restrict__ S, const float *__r
   // the P threads of one source are adjacent, so a wave's loads stay within a
   // few rows of L and S (few cache lines per load instruction)
   const int src = tid / P, part = tid % P;
-  const bool mine = src < N;
+  const bool mine = src < N && (need == nullptr || need[src] > 0);
   if (tid < N) best[tid] = ~0ull;
   __syncthreads();
   uint64_t key = ~0ull;
@@ -822,7 +960,9 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
       }
     }
   } else {
-    pool_tables(N, S, L, pool, in_pool, n_pool, tgt, scl, tgt_g, scl_g);
+    // without table outputs, only the routed sources need a target: none when
+    // every candidate is in the pool
+    pool_tables(N, S, L, pool, in_pool, n_pool, tgt, scl, tgt_g, scl_g, (tgt_g || scl_g) ? nullptr : cnt);
   }
   }  // dynamic
   lds_barrier();

@@ -171,9 +171,15 @@ class Layer:
                       None if self.ws_down is None else self.ws_down.data_ptr())
 
 
-def _workspace(nbytes: int, device) -> torch.Tensor:
-    # torch's caching allocator returns 256-byte aligned blocks (512 in practice)
-    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+def _workspace(nbytes: int, device, stream=None) -> torch.Tensor:
+    """Temporary workspace for one call.  torch's caching allocator returns 256-byte aligned
+    blocks (512 in practice).  When the call runs on another stream than the current one, the
+    block is tied to that stream too (record_stream), so the allocator does not hand it out
+    again while the call's kernels may still use it."""
+    ws = torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+    if stream is not None:
+        ws.record_stream(stream)
+    return ws
 
 
 def select_prefill(h, k_pre, logits=None, topk_ids=None, topk_w=None, top_k=None, stream=None):
@@ -300,7 +306,7 @@ def moe_forward(layer: Layer, x, phase: str = "dense", budget: int = 0, S=None, 
                      None if events is None else ctypes.cast(events, ctypes.c_void_p))
     need = lib().exfold_moe_workspace_size(ctypes.byref(ls), T, PHASE[phase], budget)
     if workspace is None:
-        workspace = _workspace(need, x.device)
+        workspace = _workspace(need, x.device, stream)
     _check(lib().exfold_moe_forward(ctypes.byref(ls), None if tb is None else ctypes.byref(tb), _ptr(x), T,
                                     PHASE[phase], budget, _ptr(y), None if dbg is None else ctypes.byref(dbg),
                                     _ptr(workspace), workspace.numel(), _stream(stream)), "exfold_moe_forward")
@@ -341,7 +347,7 @@ def moe_execute(layer: Layer, x, route_ids, route_w, y=None, debug: dict | None 
     if debug is not None:
         dbg = _Debug(*[_ptr(debug.get(f)) for f in _DEBUG_FIELDS], None)
     need = lib().exfold_execute_workspace_size(ctypes.byref(ls), T, k_out)
-    ws = _workspace(need, x.device)
+    ws = _workspace(need, x.device, stream)
     _check(lib().exfold_moe_execute(ctypes.byref(ls), _ptr(x), T, k_out, _ptr(route_ids), _ptr(route_w), _ptr(y),
                                     None if dbg is None else ctypes.byref(dbg), _ptr(ws), ws.numel(),
                                     _stream(stream)), "exfold_moe_execute")
@@ -360,7 +366,7 @@ def calibrate_projectors(layer: Layer, x_cal, lam: float = 1e-3, clip: float = 4
     h = torch.empty((N,), dtype=torch.float32, device=dev)
     stats = torch.empty((N, N, 4), dtype=torch.float64, device=dev) if with_stats else None
     need = lib().exfold_calibrate_workspace_size(ctypes.byref(ls), m, CAL_MODE[mode])
-    ws = _workspace(need, dev)
+    ws = _workspace(need, dev, stream)
     _check(lib().exfold_calibrate_projectors(ctypes.byref(ls), _ptr(x_cal), m, lam, clip, CAL_MODE[mode], _ptr(S),
                                              _ptr(L), _ptr(h), _ptr(stats), _ptr(ws), ws.numel(), _stream(stream)),
            "exfold_calibrate_projectors")
@@ -376,7 +382,7 @@ def calibrate_diagonal(layer: Layer, x_cal, lam: float = 1e-3, mode: str = "coro
     Dg = torch.empty((N, N, d), dtype=torch.float32, device=dev)
     Ld = torch.empty((N, N), dtype=torch.float32, device=dev)
     need = lib().exfold_calibrate_workspace_size(ctypes.byref(ls), m, CAL_MODE[mode])
-    ws = _workspace(need, dev)
+    ws = _workspace(need, dev, stream)
     _check(lib().exfold_calibrate_diagonal(ctypes.byref(ls), _ptr(x_cal), m, lam, CAL_MODE[mode], _ptr(Dg), _ptr(Ld),
                                            _ptr(ws), ws.numel(), _stream(stream)), "exfold_calibrate_diagonal")
     return Dg, Ld
