@@ -12,7 +12,10 @@ stand-ins (their values only steer selection, not the amount of work).
 Prints ONE JSON line: value = prefill TFLOP/s (algorithmic flops / mean
 prefill-layer time), with the decode layer's us/layer and HBM GB/s, the
 roofline of the dominant kernel (the prefill gate/up GEMM, timed live with
-HIP events on its stream) and the CPU oracle timed on a bounded sample.  The
+HIP events on its stream), the CPU oracle timed on a bounded sample (folded
+and unfolded), and a `secondary` block: the Qwen3-30B-A3B-shaped layer's
+prefill (8192 tokens, K'=4) and decode (128 tokens, D=16), folded and
+unfolded, timed in the same run.  The
 timed steps record HIP events only at the layer boundaries and around the
 dominant kernel; the per-stage breakdown in the line comes from a second,
 fully instrumented run of the same steps after the timed region.
@@ -105,6 +108,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="mixtral", choices=["mixtral", "qwen3", "glm", "qwen3-decode"])
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-secondary", action="store_true",
+                    help="skip the Qwen3-shaped prefill and decode timed after the main workload")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 1 GiB device copy (the scale for the FETCH_SIZE/WRITE_SIZE counters)")
     ap.add_argument("--prof-summary", metavar="DIR",
@@ -246,6 +251,12 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(shape, host, xs_p, (S_np, L_np, h_np), kp)
 
+    secondary = None
+    if args.workload == "mixtral" and not args.no_secondary:
+        del layer, host, x_p, x_d, y_p, y_d, ws_p, ws_d
+        torch.cuda.empty_cache()
+        secondary = secondary_configs(X, ev, args.steps, args.warmup)
+
     rec = {
         "metric": METRIC,
         "value": round(tflops, 2),
@@ -276,9 +287,71 @@ def main():
                      "kernel": " + ".join(DOMINANT) + " (prefill gate/up GEMM, fused SiLU*up)",
                      "per_launch_gflop": round(gu_flops / 1e9, 2), "avg_launch_us": round(gate_up_us, 1)},
         "cpu_baseline": cpu,
+        "secondary": secondary,
     }
     ev.close()
     print(json.dumps(rec), flush=True)
+
+
+def secondary_configs(X, ev, steps, warmup):
+    """The Qwen3-30B-A3B-shaped layer (d=2048, 128 experts, top-8, I=768, skewed router), timed in the
+    same run as the main workload: a prefill of 8192 tokens with K'=4 and a decode batch of 128 tokens
+    with a pool of D=16, each folded and unfolded (every Top-K route executed), `steps` forwards
+    after `warmup`, HIP events at each forward's start and end on the library's stream."""
+    import numpy as np
+    import torch
+    from paper_2608_24938_amd import synth
+    shape = synth.QWEN3
+    layer, _, dev = make_layer(shape, seed=0)
+    tables = tuple(dev(a) for a in synth.synthetic_tables(shape.n_experts, seed=0))
+    sptr = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    out = {}
+    for key, phase, T, budget, seed in (("qwen3_prefill", "prefill", 8192, 4, 0),
+                                        ("qwen3_decode", "decode", 128, 16, 1)):
+        x = dev(synth.tokens(shape, T, seed=seed))
+        y = torch.empty_like(x)
+        ws = torch.empty(max(X.moe_workspace_size(layer, T, phase, budget), X.moe_workspace_size(layer, T, "dense", 0)),
+                         dtype=torch.uint8, device="cuda")
+        dbg = {"offsets": torch.empty(shape.n_experts + 2, dtype=torch.int32, device="cuda")}
+
+        def timed(ph, bud):
+            for _ in range(warmup):
+                X.moe_forward(layer, x, ph, bud, *tables, y=y, workspace=ws)
+            torch.cuda.synchronize()
+            arrs = [ev.array(2) for _ in range(steps)]
+            for a in arrs:
+                ev.record(a[0], sptr)
+                X.moe_forward(layer, x, ph, bud, *tables, y=y, workspace=ws)
+                ev.record(a[1], sptr)
+            torch.cuda.synchronize()
+            return float(np.mean([ev.ms(a[0], a[1]) for a in arrs])) * 1e3
+
+        us = timed(phase, budget)
+        us_dense = timed("dense", 0)
+        X.moe_forward(layer, x, phase, budget, *tables, y=y, workspace=ws, debug=dbg)
+        counts = np.diff(dbg["offsets"].cpu().numpy()[: shape.n_experts + 1])
+        touched = int((counts > 0).sum())
+        rec = {"us_per_layer": round(us, 1), "unfolded_us_per_layer": round(us_dense, 1), "experts_touched": touched}
+        if phase == "prefill":
+            flops = prefill_flops(shape, T, budget)
+            wbytes = 3 * shape.d * shape.inter * 2 * touched + 2 * T * shape.d * 2
+            rec.update(workload=f"qwen3-30b-a3b-shaped MoE layer (d=2048, 128 experts, top-8, I=768, skewed router, "
+                                f"bf16): prefill {T} tokens K'={budget}",
+                       tflops=round(flops / (us * 1e-6) / 1e12, 2),
+                       frac_mfma_peak=round(flops / (us * 1e-6) / 1e12 / PEAK_BF16_TFLOPS, 4),
+                       algorithmic_gflop=round(flops / 1e9, 2),
+                       hbm_gbs=round(wbytes / (us * 1e-6) / 1e9, 1),
+                       frac_hbm_peak=round(wbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                       max_rows_per_expert=int(counts.max()), mean_rows_per_expert=round(float(counts[counts > 0].mean()), 1))
+        else:
+            nbytes = decode_bytes(shape, T, touched)
+            rec.update(workload=f"qwen3-30b-a3b-shaped MoE layer (bf16): decode {T} tokens, pool D={budget}",
+                       hbm_gbs=round(nbytes / (us * 1e-6) / 1e9, 1),
+                       frac_hbm_peak=round(nbytes / (us * 1e-6) / 1e9 / PEAK_HBM_GBS, 4),
+                       algorithmic_mb=round(nbytes / 1e6, 2))
+        out[key] = rec
+        log(f"{key}: {json.dumps(rec)}")
+    return out
 
 
 def cpu_baseline(shape, host, xs_p, tables, kp, target_s=15.0, probe_tokens=64):
@@ -293,6 +366,11 @@ def cpu_baseline(shape, host, xs_p, tables, kp, target_s=15.0, probe_tokens=64):
         threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [os.cpu_count()])
     except Exception:
         threads = os.cpu_count()
+    try:
+        blas = np.show_config(mode="dicts")["Build Dependencies"]["blas"]
+        blas = f"{blas.get('name')} {blas.get('version')}"
+    except Exception:
+        blas = "unknown"
     widen = synth.widen
     ref = O.Layer(w_router=widen(host["wr"]), w_gate_up=lambda e: widen(host["gu"][e]),
                   w_down=lambda e: widen(host["dn"][e]), router_bias=host["bias"],
@@ -300,10 +378,10 @@ def cpu_baseline(shape, host, xs_p, tables, kp, target_s=15.0, probe_tokens=64):
                   ws_down=None if host["sdn"] is None else widen(host["sdn"]))
     S, L, h = tables
 
-    def timed(n):
+    def timed(n, phase="prefill"):
         x = widen(xs_p[:n])
         t0 = time.perf_counter()
-        O.moe_forward(ref, x, shape.top_k, "prefill", kp, S, L, h)
+        O.moe_forward(ref, x, shape.top_k, phase, kp, S, L, h)
         return time.perf_counter() - t0
 
     n_tokens = min(probe_tokens, xs_p.shape[0])
@@ -314,9 +392,12 @@ def cpu_baseline(shape, host, xs_p, tables, kp, target_s=15.0, probe_tokens=64):
         dt = timed(n_tokens)
     flops = prefill_flops(shape, n_tokens, kp)
     log(f"cpu oracle: {n_tokens} tokens in {dt:.2f}s")
+    dt_dense = timed(n_tokens, "dense")
+    log(f"cpu oracle, unfolded: {n_tokens} tokens in {dt_dense:.2f}s")
     return {"value": flops / dt / 1e12, "unit": "TFLOP/s", "cores": int(threads), "kind": "oracle",
             "sample": f"first {n_tokens} of the {xs_p.shape[0]} prefill tokens, folded layer (float64 NumPy), "
-                      f"{dt:.2f} s wall", "seconds": round(dt, 3)}
+                      f"{dt:.2f} s wall", "seconds": round(dt, 3), "unfolded_seconds": round(dt_dense, 3),
+            "host_cpus": os.cpu_count(), "blas": blas, "blas_threads": int(threads)}
 
 
 def copy_calibration():

@@ -20,7 +20,9 @@ Mixtral-, Qwen3- and GLM-shaped prefill and decode cases) on one GPU:
 * experts touched and rows per expert (max / mean over touched experts);
 * prefill: algorithmic TFLOP/s and % of the dense bf16 MFMA peak; decode:
   algorithmic HBM bytes (touched experts' weights, router, x, y) in GB/s and %
-  of the HBM peak.
+  of the HBM peak;
+* decode: the same batch on a static pool of the same budget (tables formed
+  once), with the front-end µs it saves against the batch pool.
 
     python -m paper_2608_24938_amd.sweep [--only NAME ...] [--reps-prefill 20] [--reps-decode 100]
                                          [--md FILE] [--ceilings]
@@ -161,7 +163,41 @@ def run_config(name, wl, layer, dev, args, ev, stream, scratch):
         rec["algorithmic_mb"] = round(by / 1e6, 1)
         rec["hbm_gbs"] = round(by / (t * 1e-6) / 1e9, 1)
         rec["frac_hbm_peak"] = round(by / (t * 1e-6) / 1e9 / PEAK_HBM_GBS, 4)
+    if phase == "decode":
+        rec["static"] = static_pool_timing(X, ev, stream, layer, x, y, budget, (S, L, h), reps, scratch, st, args)
     return rec
+
+
+def static_pool_timing(X, ev, stream, layer, x, y, budget, tables, reps, scratch, st_dyn, args):
+    """The same batch on a static pool of the same budget (the D experts of largest h, per-source tables
+    formed once, Eq. appendix_decode_static_budget): cold and graph µs, experts touched, and the
+    front-end µs (Top-K, pool, tables, remap and permutation: the router-to-fold stages) against the
+    batch pool's."""
+    import torch
+    S, L, h = tables
+    _, _, tgt, scl = X.static_pool(h, budget, S, L)
+    ws = torch.empty(X.moe_workspace_size(layer, x.shape[0], "decode_static", budget), dtype=torch.uint8,
+                     device="cuda")
+    dbg = X.debug_buffers(layer, x.shape[0], "decode_static", budget, "cuda")
+
+    def fwd(events=None, debug=None):
+        X.moe_forward(layer, x, "decode_static", budget, S, L, h, y=y, workspace=ws, events=events,
+                      debug=debug, static_tables=(tgt, scl))
+
+    for _ in range(args.warmup):
+        fwd()
+    fwd(debug=dbg)
+    stream.synchronize()
+    rows = np.diff(dbg["offsets"].cpu().numpy()[: layer.n_experts + 1].astype(np.int64))
+    cold = _time(X, ev, stream, fwd, reps, scratch)
+    st = _stages(X, ev, stream, lambda a: fwd(events=a))
+    g = _capture(fwd)
+    graph = _time(X, ev, stream, g.replay, reps, None)
+    front = lambda q: q["fold"] + q["permute"]
+    return {"us_cold_median": round(float(np.median(cold)), 1), "us_graph_warm_median": round(float(np.median(graph)), 1),
+            "experts_touched": int((rows > 0).sum()), "front_us": round(front(st), 1),
+            "front_us_batch_pool": round(front(st_dyn), 1), "front_us_saved": round(front(st_dyn) - front(st), 1),
+            "stages_us": {k: round(v, 1) for k, v in st.items()}}
 
 
 def ceilings(ev, stream):
@@ -191,6 +227,20 @@ def ceilings(ev, stream):
     del big, half, dst
     torch.cuda.empty_cache()
     return out
+
+
+def markdown_static(recs):
+    rows = [r for r in recs if "static" in r]
+    if not rows:
+        return ""
+    lines = ["", "| config | batch pool: µs cold / graph, touched, front µs | static pool: µs cold / graph, touched, "
+             "front µs | front µs saved |", "|---|---|---|---|"]
+    for r in rows:
+        s = r["static"]
+        lines.append(f"| {r['config']} | {r['us_cold']['median']} / {r['us_graph_warm_median']}, {r['experts_touched']}, "
+                     f"{s['front_us_batch_pool']} | {s['us_cold_median']} / {s['us_graph_warm_median']}, "
+                     f"{s['experts_touched']}, {s['front_us']} | {s['front_us_saved']} |")
+    return "\n".join(lines) + "\n"
 
 
 def markdown(recs):
@@ -254,6 +304,7 @@ def main(argv=None):
     if args.md:
         with open(args.md, "w") as f:
             f.write(markdown(recs))
+            f.write(markdown_static(recs))
 
 
 if __name__ == "__main__":
