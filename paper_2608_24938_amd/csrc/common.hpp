@@ -107,6 +107,15 @@ __device__ __forceinline__ double wave_sum_f64(double v) {
   return (readlane_f64(v, 0) + readlane_f64(v, 16)) + (readlane_f64(v, 32) + readlane_f64(v, 48));
 }
 
+// Sum of a float over the wave in the association of wave_sum_f64.
+__device__ __forceinline__ float wave_sum_f32(float v) {
+  v += __uint_as_float(dpp_u32<0xB1>(__float_as_uint(v), 0u));
+  v += __uint_as_float(dpp_u32<0x4E>(__float_as_uint(v), 0u));
+  v += __uint_as_float(dpp_u32<0x141>(__float_as_uint(v), 0u));
+  v += __uint_as_float(dpp_u32<0x140>(__float_as_uint(v), 0u));
+  return (readlane_f32(v, 0) + readlane_f32(v, 16)) + (readlane_f32(v, 32) + readlane_f32(v, 48));
+}
+
 // Workgroup barrier that orders LDS accesses only: global stores issued before
 // it are not waited for.  For kernels whose threads exchange data through LDS
 // alone and whose global outputs are read only after the kernel.

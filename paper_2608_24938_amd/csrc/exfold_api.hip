@@ -528,38 +528,47 @@ exfold_status forward_impl(const exfold_layer *layer, const exfold_tables *table
   float *fold_w = dbg.fold_w ? dbg.fold_w : at<float>(ws, p.o_fold_w);
 
   record(dbg.events, EXFOLD_EV_START, s);
-  if (launch_router_logits(layer->dtype, x, layer->w_router, p.T, p.N, (int)layer->d, p.P, part, s) !=
-      hipSuccess)
+  // few experts (bf16): the router logits are computed inside the routing
+  // kernel (one workgroup per token), so the router stage takes no launch
+  const bool small = route_small_fits(layer->dtype, p.N, p.T);
+  if (!small && launch_router_logits(layer->dtype, x, layer->w_router, p.T, p.N, (int)layer->d, p.P, part,
+                                     s) != hipSuccess)
     return EXFOLD_ERR_DEVICE;
   record(dbg.events, EXFOLD_EV_ROUTER, s);
   const int32_t *exec_ids = fold_ids;
   const float *exec_w = fold_w;
   const float *bias = layer->router_bias;
+  // Top-K + softmax of every token, then (kp < K or fold outputs given) the
+  // prefill selection and fold
+  auto route = [&](int kp, const float *h, const float *S, const float *L, uint8_t *keep_out, int32_t *fi,
+                   float *fw, float cap, int flags, int32_t *oms = nullptr, float *omw = nullptr,
+                   int32_t *omq = nullptr, float *wret = nullptr) {
+    if (small)
+      return launch_route_small(x, layer->w_router, (int)layer->d, bias, dbg.logits, p.T, p.N, p.K, kp, h, S, L,
+                                topk_ids, topk_w, keep_out, fi, fw, s, cap, flags, oms, omw, omq, wret);
+    return launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, kp, h, S, L, topk_ids, topk_w,
+                               keep_out, nullptr, fi, fw, s, cap, flags, oms, omw, omq, wret);
+  };
   bool permuted = false;
   hipError_t e = hipSuccess;
   if (phase == EXFOLD_PHASE_DENSE) {
-    e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,
-                            topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s);
+    e = route(p.K, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0.f, 0);
     exec_ids = topk_ids;
     exec_w = topk_w;
   } else if (phase == EXFOLD_PHASE_PREFILL) {
-    e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.k_out, tables->h, tables->S,
-                            tables->L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s,
-                            tables->loss_cap, tables->fold_flags);
+    e = route(p.k_out, tables->h, tables->S, tables->L, keep, fold_ids, fold_w, tables->loss_cap,
+              tables->fold_flags);
   } else if (phase == EXFOLD_PHASE_PREFILL_DIAG) {
-    e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.k_out, tables->h, nullptr,
-                            tables->L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w, s, 0.f, 0,
-                            at<int32_t>(ws, p.o_om_src), at<float>(ws, p.o_om_w),
-                            at<int32_t>(ws, p.o_om_q), at<float>(ws, p.o_wret));
+    e = route(p.k_out, tables->h, nullptr, tables->L, keep, fold_ids, fold_w, 0.f, 0, at<int32_t>(ws, p.o_om_src),
+              at<float>(ws, p.o_om_w), at<int32_t>(ws, p.o_om_q), at<float>(ws, p.o_wret));
   } else {
     const bool stat = phase == EXFOLD_PHASE_DECODE_STATIC;
     const bool front = (int64_t)p.T * p.K <= kDecodeFrontMaxSlots;
     FrontTopK fused;
-    if (front && decode_front_fuses_topk(p.T, p.N))
+    if (!small && front && decode_front_fuses_topk(p.T, p.N))
       fused = FrontTopK{part, p.P, bias, dbg.logits, topk_ids, topk_w};
     else
-      e = launch_route_tokens(part, p.P, bias, dbg.logits, p.T, p.N, p.K, p.K, nullptr, nullptr, nullptr,
-                              topk_ids, topk_w, nullptr, nullptr, nullptr, nullptr, s);
+      e = route(p.K, nullptr, nullptr, nullptr, nullptr, nullptr, nullptr, 0.f, 0);
     if (e == hipSuccess && front) {
       // (Top-K,) pool, tables, remap and permutation in one workgroup
       const PermBuffers pb = perm_buffers(p.ex, ws, dbg.offsets, dbg.row_slot);

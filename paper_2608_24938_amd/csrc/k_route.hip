@@ -365,29 +365,46 @@ __device__ __forceinline__ void wave_topk_softmax(const float v[4], int N, int K
   my_w = (float)(z / sum);
 }
 
-__global__ __launch_bounds__(256) void route_tokens_kernel(
-    const float *__restrict__ part, int P, const float *__restrict__ bias,
-    float *__restrict__ logits_out, int T, int N, int K, int k_pre, const float *__restrict__ h,
-    const float *__restrict__ S, const float *__restrict__ L, int32_t *__restrict__ topk_ids,
-    float *__restrict__ topk_w, uint8_t *__restrict__ keep, const uint8_t *__restrict__ keep_in,
-    int32_t *__restrict__ fold_ids, float *__restrict__ fold_w, float loss_cap, int flags,
-    int32_t *__restrict__ om_src, float *__restrict__ om_w, int32_t *__restrict__ om_q,
-    float *__restrict__ wret) {
-  const int lane = threadIdx.x & 63;
-  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
-  if (t >= T) return;  // uniform per wave
-  // h of experts lane + 64 j, loaded with the logits (no load after Top-K)
-  float hv[4] = {0.f, 0.f, 0.f, 0.f};
-  if (h && !keep_in) {
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      if (lane + 64 * j < N) hv[j] = h[lane + 64 * j];
-  }
+// Per-token routing arguments (see launch_route_tokens).
+struct RouteArgs {
+  int T, N, K, k_pre;
+  const float *h, *S, *L;
+  int32_t *topk_ids;
+  float *topk_w;
+  uint8_t *keep;
+  const uint8_t *keep_in;
+  int32_t *fold_ids;
+  float *fold_w;
+  float loss_cap;
+  int flags;
+  int32_t *om_src;
+  float *om_w;
+  int32_t *om_q;
+  float *wret;
+};
+
+// One wave routes token t: Top-K and softmax of its logit row v (lane holds
+// experts lane + 64 j; have_v false: the routes are read from topk_ids/w),
+// then the prefill selection and fold.  hv: h of experts lane + 64 j.
+__device__ __forceinline__ void route_token_wave(const RouteArgs &a, int t, int lane, bool have_v,
+                                                 const float (&v)[4], const float (&hv)[4]) {
+  const int N = a.N, K = a.K, k_pre = a.k_pre;
+  const float *__restrict__ S = a.S, *__restrict__ L = a.L;
+  int32_t *__restrict__ topk_ids = a.topk_ids;
+  float *__restrict__ topk_w = a.topk_w;
+  uint8_t *__restrict__ keep = a.keep;
+  const uint8_t *__restrict__ keep_in = a.keep_in;
+  int32_t *__restrict__ fold_ids = a.fold_ids;
+  float *__restrict__ fold_w = a.fold_w;
+  const float loss_cap = a.loss_cap;
+  const int flags = a.flags;
+  int32_t *__restrict__ om_src = a.om_src;
+  float *__restrict__ om_w = a.om_w;
+  int32_t *__restrict__ om_q = a.om_q;
+  float *__restrict__ wret = a.wret;
   int my_id = 0;
   float my_w = 0.f;
-  if (part) {
-    float v[4];
-    wave_logit_row(part, P, T, N, bias, t, lane, logits_out, v);
+  if (have_v) {
     wave_topk_softmax(v, N, K, lane, my_id, my_w);
     if (lane < K) {
       topk_ids[(size_t)t * K + lane] = my_id;
@@ -516,6 +533,104 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(
   }
 }
 
+__global__ __launch_bounds__(256) void route_tokens_kernel(const float *__restrict__ part, int P,
+                                                          const float *__restrict__ bias,
+                                                          float *__restrict__ logits_out, const RouteArgs a) {
+  const int lane = threadIdx.x & 63;
+  const int t = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (t >= a.T) return;  // uniform per wave
+  // h of experts lane + 64 j, loaded with the logits (no load after Top-K)
+  float hv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (a.h && !a.keep_in) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      if (lane + 64 * j < a.N) hv[j] = a.h[lane + 64 * j];
+  }
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  if (part) wave_logit_row(part, P, a.T, a.N, bias, t, lane, logits_out, v);
+  route_token_wave(a, t, lane, part != nullptr, v, hv);
+}
+
+// Routers of at most 32 experts (bf16): one workgroup per token computes its N
+// logits (each thread a 16-byte slice of d per step against every expert,
+// then a fixed-order tree: DPP inside each wave, the four waves in order)
+// and wave 0 routes the token as route_tokens_kernel does.  One launch
+// replaces the router and Top-K kernels; W_r (<= 32 d elements) stays in L2.
+template <int NM>
+__global__ __launch_bounds__(256) void route_small_kernel(const bf16_t *__restrict__ x,
+                                                         const bf16_t *__restrict__ wr, int d,
+                                                         const float *__restrict__ bias,
+                                                         float *__restrict__ logits_out, const RouteArgs a) {
+  __shared__ float red[4][NM];
+  const int t = blockIdx.x, tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int N = a.N;
+  float hv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (wave == 0 && a.h && !a.keep_in && lane < N) hv[0] = a.h[lane];
+  float acc[NM];
+#pragma unroll
+  for (int e = 0; e < NM; ++e) acc[e] = 0.f;
+  const bf16_t *xr = x + (size_t)t * d;
+  for (int k = tid * 8; k < d; k += 256 * 8) {
+    const u32x4 xu = *reinterpret_cast<const u32x4 *>(xr + k);
+    float xf[8];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      xf[2 * q] = __uint_as_float(xu[q] << 16);
+      xf[2 * q + 1] = __uint_as_float(xu[q] & 0xffff0000u);
+    }
+    u32x4 wu[NM];
+#pragma unroll
+    for (int e = 0; e < NM; ++e)
+      if (e < N) wu[e] = *reinterpret_cast<const u32x4 *>(wr + (size_t)e * d + k);
+#pragma unroll
+    for (int e = 0; e < NM; ++e)
+      if (e < N) {
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          acc[e] = fmaf(xf[2 * q], __uint_as_float(wu[e][q] << 16), acc[e]);
+          acc[e] = fmaf(xf[2 * q + 1], __uint_as_float(wu[e][q] & 0xffff0000u), acc[e]);
+        }
+      }
+  }
+#pragma unroll
+  for (int e = 0; e < NM; ++e)
+    if (e < N) {
+      const float sum = wave_sum_f32(acc[e]);
+      if (lane == 0) red[wave][e] = sum;
+    }
+  __syncthreads();
+  if (wave != 0) return;
+  float v[4] = {0.f, 0.f, 0.f, 0.f};
+  if (lane < N) {
+    float l = ((red[0][lane] + red[1][lane]) + red[2][lane]) + red[3][lane];
+    if (bias) l += bias[lane];
+    v[0] = l;
+    if (logits_out) logits_out[(size_t)t * N + lane] = l;
+  }
+  route_token_wave(a, t, lane, true, v, hv);
+}
+
+// Up to about a thousand tokens: beyond that, the per-token reads of W_r cost
+// more than the separate router kernel (4096 Mixtral-shaped tokens: 27 us
+// against 11 + 9 us; 32 tokens: 6.8 us against 5.3 + 5.8 us).
+bool route_small_fits(int dtype, int N, int T) { return dtype == EXFOLD_BF16 && N <= 32 && T <= 1024; }
+
+hipError_t launch_route_small(const void *x, const void *w_router, int d, const float *bias,
+                              float *logits_out, int T, int N, int K, int k_pre, const float *h,
+                              const float *S, const float *L, int32_t *topk_ids, float *topk_w,
+                              uint8_t *keep, int32_t *fold_ids, float *fold_w, hipStream_t s,
+                              float loss_cap, int flags, int32_t *om_src, float *om_w, int32_t *om_q,
+                              float *wret) {
+  if (T <= 0) return hipSuccess;
+  const RouteArgs a{T, N, K, k_pre, h, S, L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w,
+                    loss_cap, flags, om_src, om_w, om_q, wret};
+  const bf16_t *xb = static_cast<const bf16_t *>(x), *wb = static_cast<const bf16_t *>(w_router);
+  if (N <= 8) route_small_kernel<8><<<T, 256, 0, s>>>(xb, wb, d, bias, logits_out, a);
+  else if (N <= 16) route_small_kernel<16><<<T, 256, 0, s>>>(xb, wb, d, bias, logits_out, a);
+  else route_small_kernel<32><<<T, 256, 0, s>>>(xb, wb, d, bias, logits_out, a);
+  return hipGetLastError();
+}
+
 hipError_t launch_route_tokens(const float *part, int P, const float *bias, float *logits_out, int T,
                                int N, int K, int k_pre, const float *h, const float *S, const float *L,
                                int32_t *topk_ids, float *topk_w, uint8_t *keep,
@@ -523,9 +638,9 @@ hipError_t launch_route_tokens(const float *part, int P, const float *bias, floa
                                hipStream_t s, float loss_cap, int flags, int32_t *om_src,
                                float *om_w, int32_t *om_q, float *wret) {
   if (T <= 0) return hipSuccess;
-  route_tokens_kernel<<<(T + 3) / 4, 256, 0, s>>>(part, P, bias, logits_out, T, N, K, k_pre, h, S, L,
-                                                  topk_ids, topk_w, keep, keep_in, fold_ids, fold_w,
-                                                  loss_cap, flags, om_src, om_w, om_q, wret);
+  const RouteArgs a{T, N, K, k_pre, h, S, L, topk_ids, topk_w, keep, keep_in, fold_ids, fold_w,
+                    loss_cap, flags, om_src, om_w, om_q, wret};
+  route_tokens_kernel<<<(T + 3) / 4, 256, 0, s>>>(part, P, bias, logits_out, a);
   return hipGetLastError();
 }
 
@@ -814,6 +929,8 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   __shared__ int wcnt[kFrontWaves][kMaxExperts];
   __shared__ unsigned long long best[kMaxExperts];
   __shared__ int scan_part[3 * kFrontScanWaves];
+  __shared__ int cand[kMaxExperts];
+  __shared__ int n_cand_sh;
   __shared__ int n_pool;
   // Threads hand data to each other through LDS only, and no global output is
   // read back here, so the phase barriers order LDS alone.
@@ -834,6 +951,7 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   const int P = kPoolThreads / N;
   const int src = tid / P, part = tid % P;
   float lv[kFrontPfCols], sv[kFrontPfCols];
+  if (tid == 0) n_cand_sh = 0;
   if (tid < N) {
     best[tid] = ~0ull;
     wsum[tid] = 0ull;
@@ -893,22 +1011,32 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   }
   lds_barrier();
   if (dynamic) {
-  if (tid < N) score[tid] = (double)(long long)wsum[tid] * (double)h_e;
-  const int n_cand = __syncthreads_count(tid < N && cnt[tid] > 0);
-  // rank of each candidate by (score desc, id asc): thread (e, part) compares e
-  // with one slice of the experts; the integer partial ranks add in any order
-  {
-    const int parts = kPoolThreads / N;
-    const int e = tid % N, pt = tid / N;
+  // candidates (experts with a routed slot) gathered in any order: their ranks
+  // come from comparisons, not from list positions
+  if (tid < N) {
+    score[tid] = (double)(long long)wsum[tid] * (double)h_e;
+    if (cnt[tid] > 0) cand[atomicAdd(&n_cand_sh, 1)] = tid;
+  }
+  lds_barrier();
+  const int n_cand = n_cand_sh;
+  // rank of each candidate by (score desc, id asc): the P = threads / n_cand
+  // threads of a candidate compare it with one slice of the candidate list
+  // each; the integer partial ranks add in any order
+  if (n_cand > 0) {
+    const int parts = kPoolThreads / n_cand;
+    const int ci = tid % n_cand, pt = tid / n_cand;
     if (pt < parts) {
-      const int chunk = (N + parts - 1) / parts;
-      const int lo = pt * chunk, hi = min(N, lo + chunk);
+      const int e = cand[ci];
+      const int chunk = (n_cand + parts - 1) / parts;
+      const int lo = pt * chunk, hi = min(n_cand, lo + chunk);
       const double sc = score[e];
       int my = 0;
-#pragma unroll 8
-      for (int o = lo; o < hi; ++o)
-        my += (cnt[o] > 0) && ((score[o] > sc) || (score[o] == sc && o < e));
-      atomicAdd(&rank_sh[e], my);
+#pragma unroll 4
+      for (int q = lo; q < hi; ++q) {
+        const int o = cand[q];
+        my += (score[o] > sc) || (score[o] == sc && o < e);
+      }
+      if (hi > lo) atomicAdd(&rank_sh[e], my);
     }
   }
   lds_barrier();

@@ -23,6 +23,16 @@ hipError_t launch_route_tokens(const float *part, int P, const float *bias, floa
                                hipStream_t s, float loss_cap = 0.f, int flags = 0,
                                int32_t *om_src = nullptr, float *om_w = nullptr,
                                int32_t *om_q = nullptr, float *wret = nullptr);
+// Router logits and the per-token steps of launch_route_tokens in one kernel, for
+// bf16 layers of at most 32 experts and batches of at most 1024 tokens
+// (route_small_fits); x [T, d], w_router [N, d].
+bool route_small_fits(int dtype, int N, int T);
+hipError_t launch_route_small(const void *x, const void *w_router, int d, const float *bias,
+                              float *logits_out, int T, int N, int K, int k_pre, const float *h,
+                              const float *S, const float *L, int32_t *topk_ids, float *topk_w,
+                              uint8_t *keep, int32_t *fold_ids, float *fold_w, hipStream_t s,
+                              float loss_cap = 0.f, int flags = 0, int32_t *om_src = nullptr,
+                              float *om_w = nullptr, int32_t *om_q = nullptr, float *wret = nullptr);
 // Decode pool (if do_pool) and per-source tables + per-slot remap (if out_ids).
 hipError_t launch_decode_pool_fold(const int32_t *ids, const float *w, int B, int N, int K, int D,
                                    const float *h, const float *S, const float *L, bool do_pool,
