@@ -1260,7 +1260,7 @@ __device__ __forceinline__ void load_cols(const InT *p, float (&v)[C]) {
   }
 }
 
-template <typename InT, typename OutT, int C>
+template <typename InT, typename OutT, int C, bool PAIRS>
 __global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y, int ksplit,
                                                      int rows, const int32_t *__restrict__ slot_row,
                                                      int k_out, int d, int shared_base,
@@ -1280,22 +1280,30 @@ __global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y,
   float acc[C];
 #pragma unroll
   for (int q = 0; q < C; ++q) acc[q] = 0.f;
-  for (int sp = 0; sp < ksplit; ++sp) {
-    // split sp of every row; with one split this is the whole sum in slot order
+  for (int sp = 0; sp < ksplit; sp += 2) {
+    // splits sp and sp + 1 of four rows at a time, all loaded before the adds
+    // (rows in slot order, the two splits in order); with one split this is
+    // the whole sum in slot order
     const InT *base = Y + sp * split + c;
+    const bool two = PAIRS && sp + 1 < ksplit;
 #pragma unroll
     for (int k0 = 0; k0 <= kMaxTopK; k0 += 4) {
       if (k0 >= nr) break;
-      float v[4][C];
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-        if (k0 + u < nr) load_cols<InT, C>(base + (long long)r[k0 + u] * d, v[u]);
+      float v[2][4][C];
 #pragma unroll
       for (int u = 0; u < 4; ++u)
         if (k0 + u < nr) {
-#pragma unroll
-          for (int q = 0; q < C; ++q) acc[q] += v[u][q];
+          load_cols<InT, C>(base + (long long)r[k0 + u] * d, v[0][u]);
+          if (two) load_cols<InT, C>(base + split + (long long)r[k0 + u] * d, v[1][u]);
         }
+#pragma unroll
+      for (int h = 0; h < 2; ++h)
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (k0 + u < nr && (h == 0 || two)) {
+#pragma unroll
+            for (int q = 0; q < C; ++q) acc[q] += v[h][u][q];
+          }
     }
   }
   OutT *o = y + (long long)i * d + c;
@@ -1314,10 +1322,16 @@ static void launch_combine_t(const InT *Y, int ksplit, int rows, const int32_t *
   // eight columns a thread once the grid covers the CUs a few times over; four below
   if ((long long)T * d >= 256LL * 256 * 8 * 4) {
     const dim3 grid(T, (d + 2047) / 2048);
-    combine_kernel<InT, OutT, 8><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
+    if (ksplit > 1)
+      combine_kernel<InT, OutT, 8, true><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
+    else
+      combine_kernel<InT, OutT, 8, false><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
   } else {
     const dim3 grid(T, (d + 1023) / 1024);
-    combine_kernel<InT, OutT, 4><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
+    if (ksplit > 1)
+      combine_kernel<InT, OutT, 4, true><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
+    else
+      combine_kernel<InT, OutT, 4, false><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
   }
 }
 

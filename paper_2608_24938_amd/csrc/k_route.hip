@@ -570,27 +570,39 @@ __global__ __launch_bounds__(256) void route_small_kernel(const bf16_t *__restri
 #pragma unroll
   for (int e = 0; e < NM; ++e) acc[e] = 0.f;
   const bf16_t *xr = x + (size_t)t * d;
-  for (int k = tid * 8; k < d; k += 256 * 8) {
-    const u32x4 xu = *reinterpret_cast<const u32x4 *>(xr + k);
-    float xf[8];
+  // two 16-byte steps of d per round, every load of the round issued first
+  constexpr int kU = NM <= 8 ? 2 : 1;
+  for (int k0 = tid * 8; k0 < d; k0 += kU * 256 * 8) {
+    u32x4 xu[kU], wu[kU][NM];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      xf[2 * q] = __uint_as_float(xu[q] << 16);
-      xf[2 * q + 1] = __uint_as_float(xu[q] & 0xffff0000u);
-    }
-    u32x4 wu[NM];
+    for (int u = 0; u < kU; ++u) {
+      const int k = k0 + u * 256 * 8;
+      if (k < d) {
+        xu[u] = *reinterpret_cast<const u32x4 *>(xr + k);
 #pragma unroll
-    for (int e = 0; e < NM; ++e)
-      if (e < N) wu[e] = *reinterpret_cast<const u32x4 *>(wr + (size_t)e * d + k);
-#pragma unroll
-    for (int e = 0; e < NM; ++e)
-      if (e < N) {
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          acc[e] = fmaf(xf[2 * q], __uint_as_float(wu[e][q] << 16), acc[e]);
-          acc[e] = fmaf(xf[2 * q + 1], __uint_as_float(wu[e][q] & 0xffff0000u), acc[e]);
-        }
+        for (int e = 0; e < NM; ++e)
+          if (e < N) wu[u][e] = *reinterpret_cast<const u32x4 *>(wr + (size_t)e * d + k);
       }
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      if (k0 + u * 256 * 8 >= d) break;
+      float xf[8];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        xf[2 * q] = __uint_as_float(xu[u][q] << 16);
+        xf[2 * q + 1] = __uint_as_float(xu[u][q] & 0xffff0000u);
+      }
+#pragma unroll
+      for (int e = 0; e < NM; ++e)
+        if (e < N) {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            acc[e] = fmaf(xf[2 * q], __uint_as_float(wu[u][e][q] << 16), acc[e]);
+            acc[e] = fmaf(xf[2 * q + 1], __uint_as_float(wu[u][e][q] & 0xffff0000u), acc[e]);
+          }
+        }
+    }
   }
 #pragma unroll
   for (int e = 0; e < NM; ++e)
