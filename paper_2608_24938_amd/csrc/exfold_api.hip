@@ -176,8 +176,10 @@ exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
   a.Y = p.direct ? nullptr : at<float>(ws, p.o_Y);
   a.y = y;
   a.direct = p.direct;
-  // rows that only the combine reads travel as bf16 (each term rounded once
-  // before the fp32 sum over the token's routes); kept rows stay fp32
+  // Rows that only the combine reads travel as bf16, unscaled: each is
+  // rounded once and the combine multiplies it by its routing weight before
+  // the fp32 sum over the token's routes.  Kept rows and split partials stay
+  // fp32 (scaled in the GEMM epilogue).
   a.y_bf16 = p.dtype == EXFOLD_BF16 && !p.direct && !keep_rows && p.dn.ksplit == 1;
   a.wide_part = at<float>(ws, p.o_wpart);
   hipEvent_t ev_mid = (events && events[EXFOLD_EV_GATE_UP])
@@ -185,7 +187,7 @@ exfold_status run_exec(const exfold_layer *L, const ExecPlan &p, const void *x,
   if (launch_expert_gemms(a, p.gu, p.dn, s, ev_mid) != hipSuccess) return EXFOLD_ERR_DEVICE;
   record(events, EXFOLD_EV_DOWN, s);
   if (!p.direct && !keep_rows) {
-    if (launch_combine(p.dtype, a.Y, a.y_bf16, p.dn.ksplit, p.rows, pb.slot_row, p.T, p.k_out, p.d,
+    if (launch_combine(p.dtype, a.Y, a.y_bf16, p.dn.ksplit, p.rows, pb.slot_row, pb.row_w, p.T, p.k_out, p.d,
                        p.t_shared > 0 ? p.R : -1, y, s) != hipSuccess)
       return EXFOLD_ERR_DEVICE;
   }

@@ -291,14 +291,12 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
             p.H[(long long)row * p.inter + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + TN / 2][r]);
           } else {
             const int n = t.nt * BN + wn * WTN + j * 32 + (lane & 31);
-            const float v = acc[i][j][r] * p.row_w[row];
             if (DIRECT)
-              p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(v);
+              p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(acc[i][j][r] * p.row_w[row]);
+            else if (p.Yh)
+              p.Yh[(long long)row * p.d + n] = f32_to_bf16(acc[i][j][r]);
             else
-              if (p.Yh)
-                p.Yh[(long long)row * p.d + n] = f32_to_bf16(v);
-              else
-                p.Y[((long long)t.ks * p.rows + row) * p.d + n] = v;
+              p.Y[((long long)t.ks * p.rows + row) * p.d + n] = acc[i][j][r] * p.row_w[row];
           }
         }
       }
@@ -557,8 +555,9 @@ __device__ __forceinline__ void store4_bf16(bf16_t *dst, float a, float b, float
   *reinterpret_cast<bf16x4 *>(dst) = v;
 }
 
-// Finished tile: gate/up writes H = SiLU(gate) * up; down scales by the row's
-// routing weight and writes y (direct), bf16 rows Yh or fp32 rows Y.
+// Finished tile: gate/up writes H = SiLU(gate) * up; down writes y (direct)
+// or fp32 rows Y scaled by the row's routing weight, or unscaled bf16 rows Yh
+// (the combine applies the weight).
 template <bool GATE_UP, bool DIRECT, int NW, bool DBL>
 __device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, int row0, int valid,
                                            const f32x16 (&acc)[kWideTM][kWideTN]) {
@@ -582,7 +581,7 @@ __device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, 
                       silu(gt[4 * g + 2]) * up[4 * g + 2], silu(gt[4 * g + 3]) * up[4 * g + 3]);
         }
     } else {
-      const float w = p.row_w[row];
+      const float w = p.Yh && !DIRECT ? 1.f : p.row_w[row];
       const int n0 = t.nt * kWideBN + wn * 32 * TN + c4;
       const long long base = DIRECT ? (long long)p.row_token[row] * p.d : (long long)row * p.d;
 #pragma unroll
@@ -605,8 +604,9 @@ __device__ __forceinline__ void wide_store(const GemmKArgs &p, const TileId &t, 
 }
 
 // Finished bf16 tile through LDS (the ring is free after the main loop): each
-// lane writes its runs of four columns (SiLU(gate) * up, or the down output
-// times the row's routing weight) into a row-major bf16 tile, and the
+// lane writes its runs of four columns (SiLU(gate) * up, or the down output,
+// scaled by the row's routing weight only when it goes straight to y) into a
+// row-major bf16 tile, and the
 // workgroup then stores whole rows 16 bytes a lane, so one store instruction
 // covers a few complete rows instead of 32 scattered 16-byte pieces.  Taken
 // for the bf16 rows of the down projection (Qwen3-shaped prefill: down 200 ->
@@ -626,7 +626,7 @@ __device__ __forceinline__ void wide_store_lds(const GemmKArgs &p, const TileId 
 #pragma unroll
   for (int i = 0; i < kWideTM; ++i) {
     const int ml = wm * 128 + i * 32 + (lane & 31);
-    const float w = (!GATE_UP && ml < valid) ? p.row_w[row0 + ml] : 1.f;
+    const float w = (!GATE_UP && DIRECT && ml < valid) ? p.row_w[row0 + ml] : 1.f;
     char *rowp = lds + ml * PITCH;
     if (GATE_UP) {
 #pragma unroll
@@ -824,7 +824,7 @@ __global__ __launch_bounds__(256) void expert_wide_fixup(const GemmKArgs p, int 
       for (int e = 0; e < 4; ++e) dst[e] = f32_to_bf16(h[e]);
     }
   } else {
-    const float rw = p.row_w[row];
+    const float rw = p.Yh && !DIRECT ? 1.f : p.row_w[row];
     for (int q = 0; q < bn / 64; ++q) {
       const int col = q * 64 + (threadIdx.x & 15) * 4;
       const float4 a = sum4(col);
@@ -994,7 +994,7 @@ __global__ __launch_bounds__(256) void expert_gemm_skinny(const GemmKArgs p) {
           if (DIRECT)
             p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(acc[j][q] * w);
           else if (p.Yh)
-            p.Yh[(long long)row * p.d + n] = f32_to_bf16(acc[j][q] * w);
+            p.Yh[(long long)row * p.d + n] = f32_to_bf16(acc[j][q]);
           else
             p.Y[((long long)t.ks * p.rows + row) * p.d + n] = acc[j][q] * w;
         }
@@ -1119,16 +1119,22 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
   }
   // Few expected tiles: split the down projection's reduction so the workgroups
   // still cover every CU.  Partial sums land in separate buffers and are added
-  // in a fixed order by the combine.
+  // in a fixed order by the combine.  Only long reductions are split: every
+  // range keeps at least kMinSplitStages stages (an intermediate size of 768
+  // split three ways ran 3 us slower per decode layer than unsplit, a 14336
+  // one split in two 20 us faster).
   const int bm = dn_skinny ? kSkM : 128;
   const int bn = dn_skinny ? kSkN : 128;
   const int kk = dn_skinny ? kSkK : kBK, fill = dn_skinny ? 3 : 2;
   *dn = GemmPlan{bm, bn, 1, 0, dn_skinny ? kGemmSkinny : kGemmTile};
   const int mt_expect = (rows + bm - 1) / bm > active ? (rows + bm - 1) / bm : active;
   const int dn_tiles = mt_expect * (d / bn);
-  if (dn_tiles < fill * cu_count) {
+  constexpr int kMinSplitStages = 8;
+  const int max_split = (inter / kk) / kMinSplitStages;
+  if (dn_tiles < fill * cu_count && max_split >= 2) {
     const int want = (fill * cu_count + dn_tiles - 1) / dn_tiles;
-    dn->ksplit = largest_divisor_at_most(inter / kk, want > 8 ? 8 : want);
+    const int cap = want < max_split ? want : max_split;
+    dn->ksplit = largest_divisor_at_most(inter / kk, cap > 8 ? 8 : cap);
   }
   dn->grid = (rows / bm + groups) * (d / bn) * dn->ksplit;
 }
@@ -1263,11 +1269,15 @@ __device__ __forceinline__ void load_cols(const InT *p, float (&v)[C]) {
 template <typename InT, typename OutT, int C, bool PAIRS>
 __global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y, int ksplit,
                                                      int rows, const int32_t *__restrict__ slot_row,
+                                                     const float *__restrict__ row_w,
                                                      int k_out, int d, int shared_base,
                                                      OutT *__restrict__ y) {
   // block (i, c): token i, columns [256 C c, 256 C (c + 1)), C per thread.  The
   // token's row indices are loaded first (one round trip), then the rows are
   // loaded four at a time and added in slot order, split partials in order.
+  // bf16 rows arrive unscaled: each is multiplied by its routing weight here,
+  // in fp32, so two routes of one token to the same expert share one rounded
+  // row and their weights add exactly as in the unrounded sum.
   const int i = blockIdx.x;
   const int c = (blockIdx.y * 256 + threadIdx.x) * C;
   if (c >= d) return;
@@ -1277,6 +1287,10 @@ __global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y,
 #pragma unroll
   for (int k = 0; k <= kMaxTopK; ++k)
     r[k] = (k < k_out) ? slot_row[(long long)i * k_out + k] : (k == k_out && shared_base >= 0) ? shared_base + i : 0;
+  constexpr bool kScale = sizeof(InT) == 2;
+  float rw[kMaxTopK + 1];
+#pragma unroll
+  for (int k = 0; k <= kMaxTopK; ++k) rw[k] = (kScale && k < nr) ? row_w[r[k]] : 1.f;
   float acc[C];
 #pragma unroll
   for (int q = 0; q < C; ++q) acc[q] = 0.f;
@@ -1302,7 +1316,7 @@ __global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y,
         for (int u = 0; u < 4; ++u)
           if (k0 + u < nr && (h == 0 || two)) {
 #pragma unroll
-            for (int q = 0; q < C; ++q) acc[q] += v[h][u][q];
+            for (int q = 0; q < C; ++q) acc[q] = kScale ? fmaf(rw[k0 + u], v[h][u][q], acc[q]) : acc[q] + v[h][u][q];
           }
     }
   }
@@ -1317,36 +1331,41 @@ __global__ __launch_bounds__(256) void combine_kernel(const InT *__restrict__ Y,
 }
 
 template <typename InT, typename OutT>
-static void launch_combine_t(const InT *Y, int ksplit, int rows, const int32_t *slot_row, int T, int k_out,
-                             int d, int shared_base, OutT *y, hipStream_t s) {
+static void launch_combine_t(const InT *Y, int ksplit, int rows, const int32_t *slot_row, const float *row_w,
+                             int T, int k_out, int d, int shared_base, OutT *y, hipStream_t s) {
   // eight columns a thread once the grid covers the CUs a few times over; four below
   if ((long long)T * d >= 256LL * 256 * 8 * 4) {
     const dim3 grid(T, (d + 2047) / 2048);
     if (ksplit > 1)
-      combine_kernel<InT, OutT, 8, true><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
+      combine_kernel<InT, OutT, 8, true><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, row_w, k_out, d,
+                                                                   shared_base, y);
     else
-      combine_kernel<InT, OutT, 8, false><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
+      combine_kernel<InT, OutT, 8, false><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, row_w, k_out, d,
+                                                                   shared_base, y);
   } else {
     const dim3 grid(T, (d + 1023) / 1024);
     if (ksplit > 1)
-      combine_kernel<InT, OutT, 4, true><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
+      combine_kernel<InT, OutT, 4, true><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, row_w, k_out, d,
+                                                                   shared_base, y);
     else
-      combine_kernel<InT, OutT, 4, false><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, k_out, d, shared_base, y);
+      combine_kernel<InT, OutT, 4, false><<<grid, 256, 0, s>>>(Y, ksplit, rows, slot_row, row_w, k_out, d,
+                                                                   shared_base, y);
   }
 }
 
 hipError_t launch_combine(int dtype, const float *Y, bool y_bf16, int ksplit, int rows,
-                          const int32_t *slot_row, int T, int k_out, int d, int shared_base, void *y,
-                          hipStream_t s) {
+                          const int32_t *slot_row, const float *row_w, int T, int k_out, int d,
+                          int shared_base, void *y, hipStream_t s) {
   if (T <= 0) return hipSuccess;
   if (dtype == EXFOLD_BF16 && y_bf16)
-    launch_combine_t<bf16_t, bf16_t>(reinterpret_cast<const bf16_t *>(Y), ksplit, rows, slot_row, T, k_out, d,
-                                     shared_base, static_cast<bf16_t *>(y), s);
+    launch_combine_t<bf16_t, bf16_t>(reinterpret_cast<const bf16_t *>(Y), ksplit, rows, slot_row, row_w, T, k_out,
+                                     d, shared_base, static_cast<bf16_t *>(y), s);
   else if (dtype == EXFOLD_BF16)
-    launch_combine_t<float, bf16_t>(Y, ksplit, rows, slot_row, T, k_out, d, shared_base,
+    launch_combine_t<float, bf16_t>(Y, ksplit, rows, slot_row, nullptr, T, k_out, d, shared_base,
                                     static_cast<bf16_t *>(y), s);
   else
-    launch_combine_t<float, float>(Y, ksplit, rows, slot_row, T, k_out, d, shared_base, static_cast<float *>(y), s);
+    launch_combine_t<float, float>(Y, ksplit, rows, slot_row, nullptr, T, k_out, d, shared_base,
+                                   static_cast<float *>(y), s);
   return hipGetLastError();
 }
 

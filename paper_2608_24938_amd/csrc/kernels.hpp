@@ -123,7 +123,7 @@ struct ExpertArgs {
   float *Y;     // [ksplit, rows, d] per-row outputs (nullptr when direct)
   void *y;      // [T, d] direct output (each token owns exactly one row)
   bool direct;
-  bool y_bf16;  // bf16 GEMMs, no split: Y holds [rows, d] bf16 rows instead
+  bool y_bf16;  // bf16 GEMMs, no split: Y holds [rows, d] unscaled bf16 rows instead
   float *wide_part;  // kGemmWide: split-remainder partial tiles, wide_partial_floats(wgs) floats
 };
 // Partial-tile scratch of a kGemmWide launch in rounds of `wgs` workgroups (the
@@ -135,9 +135,10 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
 // ev_mid (optional) is recorded between the gate_up and the down GEMM.
 hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const GemmPlan &dn,
                                hipStream_t s, hipEvent_t ev_mid = nullptr);
+// row_w: the rows' routing weights, applied here to bf16 rows (y_bf16).
 hipError_t launch_combine(int dtype, const float *Y, bool y_bf16, int ksplit, int rows,
-                          const int32_t *slot_row, int T, int k_out, int d, int shared_base, void *y,
-                          hipStream_t s);
+                          const int32_t *slot_row, const float *row_w, int T, int k_out, int d,
+                          int shared_base, void *y, hipStream_t s);
 
 // ---- diagonal projectors (k_diag.hip) ----
 // Per-pair per-dimension statistics -> Dg [N, N, d] and the diagonal loss Ld [N, N].

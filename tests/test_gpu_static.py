@@ -19,6 +19,9 @@ WIDE_BF16 = synth.LayerShape("wide-bf16", d=256, inter=128, n_experts=128, top_k
                              router_bias=True)
 SHARED_BF16 = synth.LayerShape("shared-bf16", d=384, inter=192, n_experts=64, top_k=6, shared_inter=192,
                                dtype="bf16")
+# router inside the decode front end (bf16, few tokens and experts, d a multiple of 512)
+ROUTER24_BF16 = synth.LayerShape("front-router-24", d=512, inter=256, n_experts=24, top_k=4, dtype="bf16",
+                                 router_bias=True)
 
 
 @pytest.mark.parametrize("N,D", [(8, 4), (8, 8), (8, 20), (128, 32), (128, 64), (256, 100), (3, 1), (64, 63)])
@@ -44,7 +47,7 @@ def test_static_pool_and_tables(N, D, ties):
 
 @pytest.mark.parametrize("shape,B,D", [(SMALL_BF16, 32, 4), (SMALL_BF16, 5, 8), (WIDE_BF16, 64, 16),
                                        (WIDE_BF16, 256, 32), (SHARED_BF16, 48, 8), (WIDE_BF16, 1100, 24),
-                                       (synth.TINY, 64, 3)])
+                                       (synth.TINY, 64, 3), (ROUTER24_BF16, 21, 6)])
 def test_static_forward_matches_oracle(shape, B, D):
     lp = LayerPair(shape, seed=6)
     xs = synth.tokens(shape, B, seed=6)
