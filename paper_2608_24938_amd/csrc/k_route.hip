@@ -989,10 +989,10 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   auto add_slot = [&](int j, int e, float wv) {
     sid[j] = (uint8_t)e;
     sw[j] = wv;
+    atomicAdd(&cnt[e], 1);
     if (dynamic) {
       const long long q = __double2ll_rn((double)wv * 1099511627776.0);  // 2^40
       atomicAdd(&wsum[e], (unsigned long long)q);
-      atomicAdd(&cnt[e], 1);
     }
   };
   if (lpart) {
@@ -1107,6 +1107,8 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
   }  // dynamic
   lds_barrier();
 
+  // executed rows per target: the slots of its sources
+  if (tid < N && cnt[tid] > 0) atomicAdd(&rows_of[tgt[tid]], cnt[tid]);
   // ---- remap every slot (Eq. decode_remap); retained slots copied ----
   for (int j = tid; j < slots; j += kPoolThreads) {
     const int e = sid[j];
@@ -1119,7 +1121,6 @@ __global__ __launch_bounds__(kPoolThreads) void decode_front_kernel(
     }
     sid[j] = (uint8_t)te;
     sw[j] = wn;
-    atomicAdd(&rows_of[te], 1);
   }
   lds_barrier();
 

@@ -21,11 +21,11 @@ WIDE_BF16 = synth.LayerShape("wide-bf16", d=256, inter=128, n_experts=128, top_k
 SHARED_BF16 = synth.LayerShape("shared-bf16", d=384, inter=192, n_experts=64, top_k=6, shared_inter=192,
                                dtype="bf16", m_cal=512)
 WIDE_F32 = synth.LayerShape("wide-f32", d=128, inter=64, n_experts=64, top_k=8, dtype="f32", router_bias=True)
-# decode batches whose router runs inside the front end (bf16, <= 64 tokens and 32 experts, B N <= 512,
-# d a multiple of 512), with ragged token and expert groups
-ROUTER24_BF16 = synth.LayerShape("front-router-24", d=512, inter=256, n_experts=24, top_k=4, dtype="bf16",
+# few experts (bf16, <= 32): the router, Top-K and fold in one kernel, one workgroup a token
+ROUTER24_BF16 = synth.LayerShape("router-24", d=512, inter=256, n_experts=24, top_k=4, dtype="bf16",
                                  router_bias=True)
-ROUTER8_BF16 = synth.LayerShape("front-router-8", d=1024, inter=256, n_experts=8, top_k=2, dtype="bf16")
+ROUTER8_BF16 = synth.LayerShape("router-8", d=1024, inter=256, n_experts=8, top_k=2, dtype="bf16")
+ROUTER48_BF16 = synth.LayerShape("router-48", d=768, inter=128, n_experts=48, top_k=4, dtype="bf16")
 
 
 @pytest.mark.parametrize("shape,T,k_out", [(synth.TINY, 64, 2), (synth.TINY, 1, 1), (SMALL_BF16, 200, 2),
@@ -60,13 +60,15 @@ def _forward_case(shape, T, phase, budget, seed=2):
     (WIDE_BF16, 500, "prefill", 4), (WIDE_BF16, 64, "decode", 16), (WIDE_BF16, 256, "decode", 32),
     (SHARED_BF16, 100, "prefill", 2), (SHARED_BF16, 48, "decode", 8), (WIDE_F32, 90, "prefill", 3),
     (WIDE_F32, 33, "decode", 5),
-    # 1024+ tokens: the router's many-token layout (32 tokens a workgroup for
-    # 33-128 experts), with a ragged last workgroup
+    # 1024+ tokens: the router's many-token layouts (32 tokens a workgroup for
+    # 33-128 experts, d in chunks of 256: three for the 48-expert shape), with
+    # a ragged last workgroup
     (SHARED_BF16, 1100, "prefill", 2), (WIDE_BF16, 1500, "prefill", 4), (SMALL_BF16, 1030, "prefill", 1),
+    (ROUTER48_BF16, 1050, "prefill", 2),
     # small decode batches: Top-K and softmax inside the one-workgroup front end
     (synth.TINY, 16, "decode", 4), (WIDE_BF16, 16, "decode", 16), (WIDE_F32, 20, "decode", 5),
     (SHARED_BF16, 3, "decode", 8),
-    # the router inside the decode front end; route_small_kernel for prefill and larger batches
+    # route_small_kernel (router, Top-K and fold in one kernel) for few experts
     (ROUTER24_BF16, 21, "decode", 6), (ROUTER24_BF16, 1, "decode", 2), (ROUTER8_BF16, 64, "decode", 4),
     (ROUTER8_BF16, 37, "dense", 0), (ROUTER24_BF16, 90, "decode", 10), (ROUTER24_BF16, 300, "prefill", 2),
 ])

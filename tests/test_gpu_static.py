@@ -19,8 +19,8 @@ WIDE_BF16 = synth.LayerShape("wide-bf16", d=256, inter=128, n_experts=128, top_k
                              router_bias=True)
 SHARED_BF16 = synth.LayerShape("shared-bf16", d=384, inter=192, n_experts=64, top_k=6, shared_inter=192,
                                dtype="bf16")
-# router inside the decode front end (bf16, few tokens and experts, d a multiple of 512)
-ROUTER24_BF16 = synth.LayerShape("front-router-24", d=512, inter=256, n_experts=24, top_k=4, dtype="bf16",
+# few experts (bf16, <= 32): router, Top-K and the static remap's inputs from one kernel per token
+ROUTER24_BF16 = synth.LayerShape("router-24", d=512, inter=256, n_experts=24, top_k=4, dtype="bf16",
                                  router_bias=True)
 
 
