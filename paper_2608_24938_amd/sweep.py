@@ -126,13 +126,16 @@ def run_config(name, wl, layer, dev, args, ev, stream, scratch):
     cold = _time(X, ev, stream, folded, reps, scratch)
     warm = _time(X, ev, stream, folded, reps, None)
     cold_dense = _time(X, ev, stream, dense, max(5, reps // 2), scratch)
+    # the further batches are drawn and copied to the device before any of them is timed: drawing one
+    # leaves the GPU idle long enough for its clock to drop, which the next forwards would pay
+    xb = [dev(synth.tokens(shape, T, seed=100 + i)) for i in range(N_BATCHES)]
     batch_medians = []
-    for i in range(N_BATCHES):
-        xi = dev(synth.tokens(shape, T, seed=100 + i))
-        for _ in range(2):      # untimed: the first forwards on a new batch pay one-time costs
+    for xi in xb:
+        for _ in range(args.warmup):  # untimed: the first forwards on a new batch pay one-time costs
             folded(xi)
         batch_medians.append(float(np.median(_time(X, ev, stream, lambda: folded(xi), max(5, reps // 4),
                                                    scratch))))
+    del xb
     st = _stages(X, ev, stream, lambda a: folded(events=a))
     graph = _capture(folded)
     graph_warm = _time(X, ev, stream, graph.replay, reps, None)
