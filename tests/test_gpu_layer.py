@@ -26,6 +26,9 @@ ROUTER24_BF16 = synth.LayerShape("router-24", d=512, inter=256, n_experts=24, to
                                  router_bias=True)
 ROUTER8_BF16 = synth.LayerShape("router-8", d=1024, inter=256, n_experts=8, top_k=2, dtype="bf16")
 ROUTER48_BF16 = synth.LayerShape("router-48", d=768, inter=128, n_experts=48, top_k=4, dtype="bf16")
+# the largest routing the library takes: 256 experts, top-16 (decode front end at its expert limit)
+MAX_BF16 = synth.LayerShape("max-experts", d=128, inter=128, n_experts=256, top_k=16, dtype="bf16",
+                            router_bias=True)
 
 
 @pytest.mark.parametrize("shape,T,k_out", [(synth.TINY, 64, 2), (synth.TINY, 1, 1), (SMALL_BF16, 200, 2),
@@ -68,6 +71,9 @@ def _forward_case(shape, T, phase, budget, seed=2):
     # small decode batches: Top-K and softmax inside the one-workgroup front end
     (synth.TINY, 16, "decode", 4), (WIDE_BF16, 16, "decode", 16), (WIDE_F32, 20, "decode", 5),
     (SHARED_BF16, 3, "decode", 8),
+    # 256 experts, top-16: prefill fold, decode pools below and above the candidate count, dense
+    (MAX_BF16, 90, "prefill", 5), (MAX_BF16, 24, "decode", 40), (MAX_BF16, 40, "decode", 256),
+    (MAX_BF16, 33, "dense", 0),
     # route_small_kernel (router, Top-K and fold in one kernel) for few experts
     (ROUTER24_BF16, 21, "decode", 6), (ROUTER24_BF16, 1, "decode", 2), (ROUTER8_BF16, 64, "decode", 4),
     (ROUTER8_BF16, 37, "dense", 0), (ROUTER24_BF16, 90, "decode", 10), (ROUTER24_BF16, 300, "prefill", 2),
