@@ -206,18 +206,28 @@ def static_pool_timing(X, ev, stream, layer, x, y, budget, tables, reps, scratch
 
 
 def ceilings(ev, stream):
-    """Context for the fractions: a large plain bf16 GEMM through torch (hipBLASLt), a streaming read
-    of 4 GiB through torch's reduction and a 2 GiB device copy (read + write bytes), each the median of
-    10 timed calls."""
+    """Context for the fractions: large plain bf16 GEMMs through torch (hipBLASLt) with the weights
+    stored as the layer stores them ([N_out, K], the product x W^T) and as [K, N_out] (x W), one
+    Mixtral-shaped expert (512 x 28672 x 4096, x W^T), a streaming read of 4 GiB through torch's
+    reduction and a 2 GiB device copy (read + write bytes), each the median of 10 timed calls."""
     import torch
     out = {}
     n = 8192
     a = torch.randn(n, n, device="cuda").to(torch.bfloat16)
     b = torch.randn(n, n, device="cuda").to(torch.bfloat16)
+    for name, f in (("bf16_gemm_8192_xwT_tflops", lambda: a @ b.t()), ("bf16_gemm_8192_xw_tflops", lambda: a @ b)):
+        for _ in range(3):
+            f()
+        us = _time(None, ev, stream, f, 10, None)
+        out[name] = round(2 * n ** 3 / (float(np.median(us)) * 1e-6) / 1e12, 1)
+    del a, b
+    m, nn, k = 512, 28672, 4096
+    a = torch.randn(m, k, device="cuda").to(torch.bfloat16)
+    b = torch.randn(nn, k, device="cuda").to(torch.bfloat16)
     for _ in range(3):
-        torch.matmul(a, b)
-    us = _time(None, ev, stream, lambda: torch.matmul(a, b), 10, None)
-    out["bf16_gemm_8192_tflops"] = round(2 * n ** 3 / (float(np.median(us)) * 1e-6) / 1e12, 1)
+        a @ b.t()
+    us = _time(None, ev, stream, lambda: a @ b.t(), 10, None)
+    out["bf16_gemm_mixtral_expert_xwT_tflops"] = round(2 * m * nn * k / (float(np.median(us)) * 1e-6) / 1e12, 1)
     del a, b
     big = torch.ones(1 << 30, dtype=torch.float32, device="cuda")  # 4 GiB
     for _ in range(2):
