@@ -7,7 +7,7 @@ the oracle:
 * every router logit within the float32 rounding bound of its float64 value;
 * Top-K ids (bit-exact) and softmax weights (one float32 ulp) recomputed from
   the device's logits;
-* the keep mask / pool, the folded ids and weights and the permutation,
+* the keep mask / pool (dynamic, or static with its per-source tables), the folded ids and weights and the permutation,
   bit-exact, recomputed from the device's routes;
 * the oracle's own routing from x (float64 logits) on every token: equal
   except at a near-tie of the logits;
@@ -52,7 +52,18 @@ def _check(shape, T, phase, budget, seed, tables=None):
     x = to_dev(xs)
     ws = torch.empty(X.moe_workspace_size(lp.dev, T, phase, budget), dtype=torch.uint8, device=DEV)
     dbg = X.debug_buffers(lp.dev, T, phase, budget, DEV)
-    y = X.moe_forward(lp.dev, x, phase, budget, to_dev(S), to_dev(L), to_dev(h), debug=dbg, workspace=ws)
+    if phase == "decode_static":
+        # the static pool and its per-source tables on the device, bit-exact against the oracle's
+        pool, psize, tgt, scl = X.static_pool(to_dev(h), budget, to_dev(S), to_dev(L))
+        sync()
+        s_pool = O.select_static_pool(h, budget)
+        assert int(psize.item()) == len(s_pool) and pool.cpu().numpy().tolist() == s_pool
+        rt, rs = O.decode_tables(s_pool, S, L, N)
+        np.testing.assert_array_equal(tgt.cpu().numpy(), rt)
+        np.testing.assert_array_equal(scl.cpu().numpy().view(np.uint32), rs.view(np.uint32))
+        y = X.moe_forward(lp.dev, x, phase, budget, debug=dbg, workspace=ws, static_tables=(tgt, scl))
+    else:
+        y = X.moe_forward(lp.dev, x, phase, budget, to_dev(S), to_dev(L), to_dev(h), debug=dbg, workspace=ws)
     sync()
     g = {k: v.cpu().numpy() for k, v in dbg.items()}
     y = from_dev(y)
@@ -75,6 +86,10 @@ def _check(shape, T, phase, budget, seed, tables=None):
         np.testing.assert_array_equal(g["keep"].astype(bool), keep)
         f_ids, f_w = O.fold_prefill(ids, w, keep, S, L)
         k_out = min(budget, K)
+    elif phase == "decode_static":
+        f_ids, f_w, _, _ = O.fold_decode(ids, w, s_pool, S, L, N)
+        assert set(np.unique(g["fold_ids"]).tolist()) <= set(s_pool)
+        k_out = K
     else:
         pool, cand = O.select_decode_pool(ids, w, h, N, budget)
         n = int(g["pool_size"][0])
@@ -132,6 +147,13 @@ def test_glm_decode(B, D):
 @pytest.mark.parametrize("B,D", [(1, 16), (8, 16), (64, 16), (512, 16), (128, 32), (1, 64), (64, 64), (512, 64)])
 def test_qwen3_decode_sweep(B, D):
     _check(synth.QWEN3_DECODE, B, "decode", D, seed=3 * B + D)
+
+
+@pytest.mark.parametrize("shape,B,D", [(synth.QWEN3_DECODE, 128, 16), (synth.QWEN3_DECODE, 1, 64),
+                                       (synth.GLM45, 64, 32), (synth.MIXTRAL, 32, 4)])
+def test_static_decode(shape, B, D):
+    """Static decode pool (TopK of the norm proxy, tables precomputed once) at the full sizes."""
+    _check(shape, B, "decode_static", D, seed=5 * B + D)
 
 
 CAL_TOL = 1e-2   # bf16 expert outputs: H rounded to bf16 before the down projection
