@@ -397,7 +397,11 @@ constexpr int kWideSmemElems = kWideStages * (kWide / 2 + 2 * kWideBN) * kWideBK
 // All waves of the workgroup call it; it ends with every load landed and a
 // barrier, so the ring may be refilled right after.  DBL: the 128 x 512 tail
 // tile (one row of NW waves) instead of 256 x 256 (two rows of NW / 2).
-template <bool GATE_UP, int BK, int STAGES, int NW, bool DBL>
+// TMV: the calling wave's 32-row blocks that hold rows of the group (the
+// others are padding: their fragments are not read and their MFMAs not
+// issued, so their accumulators stay zero); the wave still loads its share of
+// every stage and takes every barrier.
+template <bool GATE_UP, int BK, int STAGES, int NW, bool DBL, int TMV>
 __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &t, int row0, int valid,
                                               int k0, int k1, bf16_t *smem,
                                               f32x16 (&acc)[kWideTM][kWideTN]) {
@@ -406,6 +410,7 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
   constexpr int WM = DBL ? 1 : 2, WN = NW / WM;
   constexpr int BM = 128 * WM, TM = kWideTM, TN = kWideTN, BN = 32 * TN * WN;
   static_assert(NW == kWideWaves, "accumulator shape");
+  static_assert(TMV >= 0 && TMV <= TM, "valid row blocks");
   constexpr int STAGE = (BM + BN) * BK;          // elements of one stage (A rows, then B rows)
   constexpr int CPR = BK / 8;                    // 16-byte chunks per row
   constexpr int RPB = 64 / CPR;                  // rows per 1 KiB block
@@ -477,14 +482,15 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
     const bf16_t *As_ = smem + (BUF) * STAGE;                                                  \
     const bf16_t *Bs_ = As_ + BM * BK;                                                         \
     const int ch_ = (S_) * 2 + (lane >> 5);                                                    \
-    _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_) A_[i_] = *reinterpret_cast<const bf16x8 *>( \
+    _Pragma("unroll") for (int i_ = 0; i_ < TMV; ++i_) A_[i_] = *reinterpret_cast<const bf16x8 *>( \
         As_ + a_row[i_] * BK + wide_slot<BK>(a_row[i_], ch_) * 8);                             \
-    _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) B_[j_] = *reinterpret_cast<const bf16x8 *>( \
-        Bs_ + b_row[j_] * BK + wide_slot<BK>(b_row[j_], ch_) * 8);                             \
+    if (TMV > 0)                                                                               \
+      _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) B_[j_] = *reinterpret_cast<const bf16x8 *>( \
+          Bs_ + b_row[j_] * BK + wide_slot<BK>(b_row[j_], ch_) * 8);                           \
   } while (0)
 #define EXF_W_MMA(A_, B_)                                                                      \
   do {                                                                                         \
-    _Pragma("unroll") for (int i_ = 0; i_ < TM; ++i_)                                          \
+    _Pragma("unroll") for (int i_ = 0; i_ < TMV; ++i_)                                         \
         _Pragma("unroll") for (int j_ = 0; j_ < TN; ++j_) acc[i_][j_] =                        \
             __builtin_amdgcn_mfma_f32_32x32x16_bf16(B_[j_], A_[i_], acc[i_][j_], 0, 0, 0);     \
   } while (0)
@@ -521,13 +527,15 @@ __device__ __forceinline__ void wide_tile_mma(const GemmKArgs &p, const TileId &
         EXF_W_FRAGS(fa[s_ & 1], fb[s_ & 1], buf, s_);
         if (s_ > 0) {
           EXF_W_MMA(fa[(s_ - 1) & 1], fb[(s_ - 1) & 1]);
-          // one LDS read after each of the first TM + TN MFMAs
+          // one LDS read after each of the first MFMAs
+          constexpr int MF = TMV * TN, RD = TMV > 0 ? TMV + TN : 0, PAIRS = MF < RD ? MF : RD;
 #pragma unroll
-          for (int g_ = 0; g_ < TM + TN; ++g_) {
+          for (int g_ = 0; g_ < PAIRS; ++g_) {
             __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
             __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
           }
-          __builtin_amdgcn_sched_group_barrier(0x008, TM * TN - TM - TN, 0);
+          if (MF > PAIRS) __builtin_amdgcn_sched_group_barrier(0x008, MF - PAIRS, 0);
+          if (RD > PAIRS) __builtin_amdgcn_sched_group_barrier(0x100, RD - PAIRS, 0);
         } else if (kt > k0) {
           EXF_W_MMA(fa[1], fb[1]);
         }
@@ -743,9 +751,23 @@ __device__ __forceinline__ void wide_gemm(const GemmKArgs &p, int G, bf16_t *sme
   }
   const int row0 = p.offsets[t.g] + t.mt * kWide;
   f32x16 acc[kWideTM][kWideTN];
+  // the wave's 32-row blocks that hold rows of the group (wave-uniform)
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  auto blocks = [&](int valid, int wm) { return max(0, min(kWideTM, (valid - wm * 128 + 31) >> 5)); };
+#define EXF_W_MAIN(DBL_, TMV_) \
+  wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, DBL_, TMV_>(p, t, row0, valid, k0, k1, smem, acc)
+#define EXF_W_DISPATCH(DBL_, TMV_VAL)                                                          \
+  switch (TMV_VAL) {                                                                           \
+    case 4: EXF_W_MAIN(DBL_, 4); break;                                                        \
+    case 3: EXF_W_MAIN(DBL_, 3); break;                                                        \
+    case 2: EXF_W_MAIN(DBL_, 2); break;                                                        \
+    case 1: EXF_W_MAIN(DBL_, 1); break;                                                        \
+    default: EXF_W_MAIN(DBL_, 0); break;                                                       \
+  }
+  static_assert(kWideTM == 4, "the dispatch below covers 0 .. 4 valid row blocks");
   if (__builtin_amdgcn_readfirstlane(t.dbl)) {
     const int valid = min(kWide / 2, p.offsets[t.g + 1] - row0);
-    wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, true>(p, t, row0, valid, k0, k1, smem, acc);
+    EXF_W_DISPATCH(true, blocks(valid, 0))
     if (part)
       wide_store_partial<true>(part, acc);
     else if (!GATE_UP && !DIRECT && p.Yh)
@@ -754,7 +776,7 @@ __device__ __forceinline__ void wide_gemm(const GemmKArgs &p, int G, bf16_t *sme
       wide_store<GATE_UP, DIRECT, NW, true>(p, t, row0, valid, acc);
   } else {
     const int valid = min(kWide, p.offsets[t.g + 1] - row0);
-    wide_tile_mma<GATE_UP, kWideBK, kWideStages, NW, false>(p, t, row0, valid, k0, k1, smem, acc);
+    EXF_W_DISPATCH(false, blocks(valid, wave / (NW / 2)))
     if (part)
       wide_store_partial<false>(part, acc);
     else if (!GATE_UP && !DIRECT && p.Yh)
@@ -762,6 +784,8 @@ __device__ __forceinline__ void wide_gemm(const GemmKArgs &p, int G, bf16_t *sme
     else
       wide_store<GATE_UP, DIRECT, NW, false>(p, t, row0, valid, acc);
   }
+#undef EXF_W_MAIN
+#undef EXF_W_DISPATCH
 }
 
 
