@@ -90,7 +90,10 @@ __device__ __forceinline__ bool decode_tile(const GemmKArgs &p, int wg, TileId &
 // ---------------------------------------------------------------------------
 // Macro-tile kernel.
 // ---------------------------------------------------------------------------
-template <int BM, int BN, int STAGES, bool GATE_UP, bool DIRECT>
+// PLAIN: one group of p.rows rows read in order (no offsets, tile list or
+// gather), partial sums of split ks written unscaled to Y[ks] (a plain
+// x W^T with a split reduction: the router logits of large batches).
+template <int BM, int BN, int STAGES, bool GATE_UP, bool DIRECT, bool PLAIN = false>
 __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
   constexpr int WTM = BM / 2, WTN = BN / 2;
   constexpr int TM = WTM / 32, TN = WTN / 32;
@@ -103,10 +106,25 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
   const int wm = wave >> 1, wn = wave & 1;
 
   TileId t;
-  if (!decode_tile(p, blockIdx.x, t)) return;
-  const int row0 = p.offsets[t.g] + t.mt * BM;
-  const int valid = min(BM, p.offsets[t.g + 1] - row0);
-  const bf16_t *Wg = (t.g < p.n_experts) ? p.W + (long long)t.g * p.w_stride : p.Ws;
+  int row0, valid;
+  const bf16_t *Wg;
+  if constexpr (PLAIN) {
+    const int mt_n = (p.rows + BM - 1) / BM, total = mt_n * p.n_tiles * p.ksplit;
+    if ((int)blockIdx.x >= total) return;
+    const int L = xcd_remap(blockIdx.x, total);
+    t.g = 0;
+    t.mt = L % mt_n;
+    t.ks = (L / mt_n) % p.ksplit;
+    t.nt = L / mt_n / p.ksplit;
+    row0 = t.mt * BM;
+    valid = min(BM, p.rows - row0);
+    Wg = p.W;
+  } else {
+    if (!decode_tile(p, blockIdx.x, t)) return;
+    row0 = p.offsets[t.g] + t.mt * BM;
+    valid = min(BM, p.offsets[t.g + 1] - row0);
+    Wg = (t.g < p.n_experts) ? p.W + (long long)t.g * p.w_stride : p.Ws;
+  }
 
   // global source of this thread's 16-byte chunks (row r = c / 8, chunk q = c % 8)
   // A rows past the group's end are not loaded (their outputs are never stored):
@@ -291,7 +309,9 @@ __global__ __launch_bounds__(256, 1) void expert_gemm_tile(const GemmKArgs p) {
             p.H[(long long)row * p.inter + n] = f32_to_bf16(silu(acc[i][j][r]) * acc[i][j + TN / 2][r]);
           } else {
             const int n = t.nt * BN + wn * WTN + j * 32 + (lane & 31);
-            if (DIRECT)
+            if (PLAIN)
+              p.Y[((long long)t.ks * p.rows + row) * p.d + n] = acc[i][j][r];
+            else if (DIRECT)
               p.y[(long long)p.row_token[row] * p.d + n] = f32_to_bf16(acc[i][j][r] * p.row_w[row]);
             else if (p.Yh)
               p.Yh[(long long)row * p.d + n] = f32_to_bf16(acc[i][j][r]);
@@ -1258,6 +1278,34 @@ hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const Ge
         expert_gemm_tile<128, 128, 2, false, false><<<dn.grid, 256, 0, s>>>(da);
     }
   }
+  return hipGetLastError();
+}
+
+int plain_gemm_splits(int M, int N, int K, int cu_count) {
+  if (M <= 0 || N % 128 != 0 || K % kBK != 0) return 0;
+  const int tiles = (M + 127) / 128 * (N / 128);
+  int P = 1;
+  // split the reduction until the tiles cover the CUs, every range at least
+  // four stages of kBK
+  while (tiles * P < cu_count && P < 8 && K % (2 * P * kBK) == 0 && K / (2 * P) >= 4 * kBK) P *= 2;
+  return P;
+}
+
+hipError_t launch_plain_gemm_nt(const void *A, const void *W, int M, int N, int K, int P, float *part,
+                                hipStream_t s) {
+  GemmKArgs g{};
+  g.A = static_cast<const bf16_t *>(A);
+  g.lda = K;
+  g.W = static_cast<const bf16_t *>(W);
+  g.ldw = K;
+  g.rows = M;
+  g.d = N;
+  g.n_tiles = N / 128;
+  g.ksplit = P;
+  g.kc = K / P;
+  g.Y = part;
+  const int grid = (M + 127) / 128 * g.n_tiles * P;
+  expert_gemm_tile<128, 128, 2, false, false, true><<<grid, 256, 0, s>>>(g);
   return hipGetLastError();
 }
 

@@ -217,8 +217,16 @@ __global__ __launch_bounds__(64 * NW) void router_logits_lds(const bf16_t *__res
 // Blocks of the all-experts layout at or above which the d axis is not split.
 constexpr int kRouterWideBlocks = 64;
 
+// Many tokens and a multiple of 128 experts: the router is a plain MFMA GEMM
+// on 128 x 128 tiles with its reduction split so the tiles cover the CUs
+// (8192 tokens x 128 experts x 2048: 256 tiles of 512-deep reductions).
+static bool router_tiled(int T, int N, int d) {
+  return (T + 15) / 16 >= kRouterWideBlocks && plain_gemm_splits(T, N, d, 256) > 0;
+}
+
 int router_splits(int dtype, int T, int N, int d) {
   if (dtype != EXFOLD_BF16 || T <= 0) return 1;
+  if (router_tiled(T, N, d)) return plain_gemm_splits(T, N, d, 256);
   const int tb = (T + 15) / 16;
   if (tb >= kRouterWideBlocks) return 1;
   const int nb = (N + 15) / 16;
@@ -265,6 +273,10 @@ hipError_t launch_router_logits(int dtype, const void *x, const void *w_router, 
     const bf16_t *xb = static_cast<const bf16_t *>(x);
     const bf16_t *wb = static_cast<const bf16_t *>(w_router);
     const int tb = (T + 15) / 16;
+    if (router_tiled(T, N, d)) {
+      if (P != plain_gemm_splits(T, N, d, 256)) return hipErrorInvalidValue;
+      return launch_plain_gemm_nt(xb, wb, T, N, d, P, part, s);
+    }
     if (tb < kRouterWideBlocks) {
       // 16 tokens x 16 experts x d/P per block
       const dim3 grid(tb, (N + 15) / 16, P);

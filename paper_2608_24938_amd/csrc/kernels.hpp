@@ -135,6 +135,12 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
 // ev_mid (optional) is recorded between the gate_up and the down GEMM.
 hipError_t launch_expert_gemms(const ExpertArgs &a, const GemmPlan &gu, const GemmPlan &dn,
                                hipStream_t s, hipEvent_t ev_mid = nullptr);
+// Plain bf16 product part[P][M][N] = partial sums over P equal reduction
+// ranges of A[M, K] W[N, K]^T (fp32, MFMA 128x128 tiles).  plain_gemm_splits
+// gives P for the shape (0: N % 128 != 0 or K % 64 != 0, not supported).
+int plain_gemm_splits(int M, int N, int K, int cu_count);
+hipError_t launch_plain_gemm_nt(const void *A, const void *W, int M, int N, int K, int P, float *part,
+                                hipStream_t s);
 // row_w: the rows' routing weights, applied here to bf16 rows (y_bf16).
 hipError_t launch_combine(int dtype, const float *Y, bool y_bf16, int ksplit, int rows,
                           const int32_t *slot_row, const float *row_w, int T, int k_out, int d,

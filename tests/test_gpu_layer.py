@@ -29,6 +29,10 @@ ROUTER48_BF16 = synth.LayerShape("router-48", d=768, inter=128, n_experts=48, to
 # the largest routing the library takes: 256 experts, top-16 (decode front end at its expert limit)
 MAX_BF16 = synth.LayerShape("max-experts", d=128, inter=128, n_experts=256, top_k=16, dtype="bf16",
                             router_bias=True)
+# 1024+ tokens and a multiple of 128 experts: the router as a plain tiled GEMM whose
+# reduction is split in four (partial sums added in order by the Top-K kernel)
+ROUTER_SPLIT_BF16 = synth.LayerShape("router-split", d=1024, inter=128, n_experts=128, top_k=8, dtype="bf16",
+                                     router_bias=True)
 
 
 @pytest.mark.parametrize("shape,T,k_out", [(synth.TINY, 64, 2), (synth.TINY, 1, 1), (SMALL_BF16, 200, 2),
@@ -64,10 +68,10 @@ def _forward_case(shape, T, phase, budget, seed=2):
     (SHARED_BF16, 100, "prefill", 2), (SHARED_BF16, 48, "decode", 8), (WIDE_F32, 90, "prefill", 3),
     (WIDE_F32, 33, "decode", 5),
     # 1024+ tokens: the router's many-token layouts (32 tokens a workgroup for
-    # 33-128 experts, d in chunks of 256: three for the 48-expert shape), with
-    # a ragged last workgroup
+    # 33-127 experts, d in chunks of 256: three for the 48-expert shape; 128 x
+    # 128 MFMA tiles for multiples of 128 experts), with a ragged last tile
     (SHARED_BF16, 1100, "prefill", 2), (WIDE_BF16, 1500, "prefill", 4), (SMALL_BF16, 1030, "prefill", 1),
-    (ROUTER48_BF16, 1050, "prefill", 2),
+    (ROUTER48_BF16, 1050, "prefill", 2), (ROUTER_SPLIT_BF16, 1100, "prefill", 3), (MAX_BF16, 1030, "prefill", 5),
     # small decode batches: Top-K and softmax inside the one-workgroup front end
     (synth.TINY, 16, "decode", 4), (WIDE_BF16, 16, "decode", 16), (WIDE_F32, 20, "decode", 5),
     (SHARED_BF16, 3, "decode", 8),
