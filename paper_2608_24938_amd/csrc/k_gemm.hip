@@ -1130,18 +1130,25 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
   const int active = active_groups < 1 ? 1 : active_groups;
   // Few rows per retained expert (decode): skinny 32x64 tiles stream the weights
   // through many small workgroups; otherwise 128x128 tiles.  The gate/up
-  // projection keeps 128-row tiles once the experts hold more than about 24
-  // rows each and those tiles already cover the CUs: skinny tiles then read the
-  // weights of a busy expert more than once.
+  // projection takes 128-row tiles once the experts hold more than about 24
+  // rows each, even where those tiles do not cover the CUs: skinny tiles then
+  // read the weights of a busy expert more than once (Qwen3-shaped decode, 128
+  // tokens on a pool of 16: 80.8 against 85.6 us per layer).
   const bool sk_shapes = inter % 128 == 0 && d % 64 == 0;
-  const int mt128 = (rows + 127) / 128 > active ? (rows + 127) / 128 : active;
-  const bool gu_skinny = sk_shapes && (rows <= 24 * active || mt128 * (inter / 64) < cu_count);
+  const bool gu_skinny = sk_shapes && rows <= 24 * active;
   // Many rows per retained expert (prefill, at least 128 on average): wide
   // tiles.  With the 128-row tail tiles a skewed load pays at most half a tile
   // per group: the Qwen3-shaped prefill (8192 tokens, K' = 4, 98 of 128 experts
   // busy, 334 rows on average, 3974 at most) runs 19% faster than on 128x128.
-  const bool gu_wide = !gu_skinny && inter % kWideBN == 0 && d % 128 == 0 && 2 * rows >= kWide * active;
-  const bool dn_skinny = sk_shapes && rows <= 64 * active;
+  // Fewer than a quarter round of wide tiles (then split four ways or more)
+  // loses to 128x128 tiles (Qwen3-shaped decode, 256 tokens on a pool of 16,
+  // 48 wide tiles: 130.8 against 103.8 us per layer).
+  const bool gu_wide = !gu_skinny && inter % kWideBN == 0 && d % 128 == 0 && 2 * rows >= kWide * active &&
+                       (long long)(rows / 128) * (inter / kWideBN) * 4 >= cu_count;
+  // The down projection keeps skinny tiles up to about 48 rows per expert (at
+  // 64, 128x128 tiles: Qwen3-shaped decode, 256 tokens on a pool of 32, 115
+  // against 125 us per layer).
+  const bool dn_skinny = sk_shapes && rows <= 48 * active;
   if (gu_skinny) {
     *gu = GemmPlan{kSkM, kSkN, 1, 0, kGemmSkinny};
     gu->grid = (rows / kSkM + groups) * (inter / (kSkN / 2));  // >= sum of ceil(rows_g / 32) tiles
@@ -1154,9 +1161,11 @@ void plan_expert_gemms(int dtype, int rows, int groups, int active_groups, int d
     *gu = GemmPlan{128, 128, 1, 0, kGemmTile};
     gu->grid = (rows / 128 + groups) * (inter / 64);
   }
-  // Down projection on the wide tile where the gate/up projection takes it and
-  // the tiles (at least rows / 256 per 256 output columns) fill one round.
-  if (!dn_skinny && gu_wide && d % (2 * kWideBN) == 0 && (long long)(rows / kWide) * (d / kWide) >= cu_count) {
+  // Down projection on the wide tile where the gate/up projection takes it,
+  // also when its tiles do not fill one round (they then all run split along
+  // the reduction: Qwen3-shaped decode, 512 tokens on a pool of 32, 150.7
+  // against 160.0 us per layer with 128x128 tiles).
+  if (!dn_skinny && gu_wide && d % (2 * kWideBN) == 0) {
     *dn = GemmPlan{kWide / 2, kWideBN, 1, 0, kGemmWide, cu_count};
     dn->grid = (rows / 128 + groups) * (d / (2 * kWideBN)) + cu_count;
     return;

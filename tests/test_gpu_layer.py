@@ -372,12 +372,13 @@ def _wide_split(tiles, G, KT):
 # for both GEMMs: 75 units = 300 tiles (44 split 5 ways for gate/up, 4 for
 # down; tails of each kind), 96 = 384 (128 split twice, the largest split
 # remainder), 100 = 400 (144 left whole)
-SPLIT_COUNTS = {75: [1300, 1200, 1100, 1000, 1400, 1024, 1100, 1100],
+SPLIT_COUNTS = {32: [512] * 8,   # 128 tiles: no whole round, every tile split in two
+                75: [1300, 1200, 1100, 1000, 1400, 1024, 1100, 1100],
                 96: [1500, 1500, 1537, 1538, 1290, 1300, 1400, 1540],
                 100: [1500, 1500, 1537, 1538, 1290, 1300, 1400, 2101]}
 
 
-@pytest.mark.parametrize("units,k_out", [(75, 1), (75, 2), (96, 1), (100, 2)])
+@pytest.mark.parametrize("units,k_out", [(32, 2), (75, 1), (75, 2), (96, 1), (100, 2)])
 def test_execute_wide_split_remainder(units, k_out):
     shape = SPLIT_SHAPE
     counts = np.array(SPLIT_COUNTS[units])

@@ -35,7 +35,9 @@ GLM = dict(d=4096, inter=1408, n=128, k=8, shared=1408)
     (MIXTRAL, 8192, 8, WIDE, WIDE),
     (MIXTRAL, 64, 4, SKINNY, SKINNY),        # decode, 32 tokens, pool of 4
     (QWEN3, 32768, 128, WIDE, WIDE),         # prefill, 8192 tokens, K' = 4
-    (QWEN3, 1024, 16, SKINNY, SKINNY),       # decode, 128 tokens, pool of 16
+    (QWEN3, 1024, 16, TILE, TILE),           # decode, 128 tokens, pool of 16 (64 rows per expert)
+    (QWEN3, 1024, 64, SKINNY, SKINNY),       # decode, 128 tokens, pool of 64 (16 rows per expert)
+    (QWEN3, 4096, 32, WIDE, WIDE),           # decode, 512 tokens, pool of 32 (wide down without a full round)
     (GLM, 64 * 8 + 64, 33, SKINNY, SKINNY),  # decode with the shared expert
     (GLM, 4096 * 4 + 4096, 129, TILE, TILE),  # I = 1408 splits into no 256-wide pairs
 ])
