@@ -144,7 +144,9 @@ def test_glm_decode(B, D):
     _check(synth.GLM45, B, "decode", D, seed=B + D)
 
 
-@pytest.mark.parametrize("B,D", [(1, 16), (8, 16), (64, 16), (512, 16), (128, 32), (1, 64), (64, 64), (512, 64)])
+# (128, 16), (256, 32): 128x128 tiles for both projections; (512, 16), (512, 32): wide tiles for both
+@pytest.mark.parametrize("B,D", [(1, 16), (8, 16), (64, 16), (128, 16), (512, 16), (128, 32), (256, 32), (512, 32),
+                                 (1, 64), (64, 64), (512, 64)])
 def test_qwen3_decode_sweep(B, D):
     _check(synth.QWEN3_DECODE, B, "decode", D, seed=3 * B + D)
 
