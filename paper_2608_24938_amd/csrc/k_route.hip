@@ -568,6 +568,8 @@ __global__ __launch_bounds__(256) void route_tokens_kernel(const float *__restri
 // then a fixed-order tree: DPP inside each wave, the four waves in order)
 // and wave 0 routes the token as route_tokens_kernel does.  One launch
 // replaces the router and Top-K kernels; W_r (<= 32 d elements) stays in L2.
+constexpr int kRouteSmallMaxT = 1024;  // route_small_kernel: one workgroup per token up to this batch
+
 template <int NM>
 __global__ __launch_bounds__(256) void route_small_kernel(const bf16_t *__restrict__ x,
                                                          const bf16_t *__restrict__ wr, int d,
@@ -637,7 +639,97 @@ __global__ __launch_bounds__(256) void route_small_kernel(const bf16_t *__restri
 // Up to about a thousand tokens: beyond that, the per-token reads of W_r cost
 // more than the separate router kernel (4096 Mixtral-shaped tokens: 27 us
 // against 11 + 9 us; 32 tokens: 6.8 us against 5.3 + 5.8 us).
-bool route_small_fits(int dtype, int N, int T) { return dtype == EXFOLD_BF16 && N <= 32 && T <= 1024; }
+// Beyond that batch size (few experts, many tokens): one workgroup per 16
+// tokens takes their logits over the whole of d with 16x16x32 MFMAs (KS waves
+// on consecutive ranges of d, the partial tiles added in wave order through
+// LDS; the grid of the d-split router at these sizes), adds the bias, and its
+// waves then route the tokens (route_token_wave): no Top-K launch and no logit
+// rows in memory.  Every workgroup reads all of W_r (64 KiB for the
+// Mixtral-shaped layer), so this is for few experts only (at 128 experts the
+// same kernel made decode layers 13-27 us slower than the d-split router).
+template <int NT, int KS>
+__global__ __launch_bounds__(64 * KS) void route_block_kernel(const bf16_t *__restrict__ x,
+                                                              const bf16_t *__restrict__ wr, int d,
+                                                              const float *__restrict__ bias,
+                                                              float *__restrict__ logits_out, const RouteArgs a) {
+  __shared__ float red[KS][NT * 4][64];
+  __shared__ float lg[16][16 * NT];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63;
+  const int T = a.T, N = a.N;
+  const int t0 = blockIdx.x * 16;
+  const int kq = (lane >> 4) * 8;
+  f32x4 acc[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) acc[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bf16_t *wrow[NT];
+  bool live[NT];
+#pragma unroll
+  for (int j = 0; j < NT; ++j) {
+    const int e = j * 16 + (lane & 15);
+    live[j] = e < N;
+    wrow[j] = wr + (size_t)(live[j] ? e : 0) * d + kq;
+  }
+  const bf16_t *xa = x + (size_t)min(t0 + (lane & 15), T - 1) * d + kq;
+  const int steps = d / 32;
+  const int s0 = wave * steps / KS, s1 = (wave + 1) * steps / KS;
+  bf16x8 zero;
+#pragma unroll
+  for (int q = 0; q < 8; ++q) zero[q] = (__bf16)0.0f;
+  int st = s0;
+  for (; st + 2 <= s1; st += 2) {
+    const int k = st * 32;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(xa + k);
+    const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(xa + k + 32);
+    bf16x8 b0[NT], b1[NT];
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      b0[j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
+      b1[j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k + 32);
+    }
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, live[j] ? b0[j] : zero, acc[j], 0, 0, 0);
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, live[j] ? b1[j] : zero, acc[j], 0, 0, 0);
+    }
+  }
+  if (st < s1) {
+    const int k = st * 32;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(xa + k);
+#pragma unroll
+    for (int j = 0; j < NT; ++j) {
+      const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, live[j] ? b0 : zero, acc[j], 0, 0, 0);
+    }
+  }
+  // accumulator i of lane l: token (l / 16) * 4 + i, expert 16 j + l % 16
+#pragma unroll
+  for (int j = 0; j < NT; ++j)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) red[wave][j * 4 + i][lane] = acc[j][i];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < NT * 4 * 64; idx += 64 * KS) {
+    const int ji = idx >> 6, l = idx & 63;
+    float v = red[0][ji][l];
+#pragma unroll
+    for (int w = 1; w < KS; ++w) v += red[w][ji][l];
+    const int tl = (l >> 4) * 4 + (ji & 3), e = (ji >> 2) * 16 + (l & 15);
+    if (e < N) {
+      if (bias) v += bias[e];
+      lg[tl][e] = v;
+      if (logits_out && t0 + tl < T) logits_out[(size_t)(t0 + tl) * N + e] = v;
+    }
+  }
+  __syncthreads();
+  float hv[4] = {0.f, 0.f, 0.f, 0.f};
+  if (a.h && !a.keep_in && lane < N) hv[0] = a.h[lane];
+  for (int tl = wave; tl < 16 && t0 + tl < T; tl += KS) {
+    float v[4] = {0.f, 0.f, 0.f, 0.f};
+    if (lane < N) v[0] = lg[tl][lane];
+    route_token_wave(a, t0 + tl, lane, true, v, hv);
+  }
+}
+
+bool route_small_fits(int dtype, int N, int T) { return dtype == EXFOLD_BF16 && N <= 32; }
 
 hipError_t launch_route_small(const void *x, const void *w_router, int d, const float *bias,
                               float *logits_out, int T, int N, int K, int k_pre, const float *h,
@@ -649,7 +741,11 @@ hipError_t launch_route_small(const void *x, const void *w_router, int d, const 
   const RouteArgs a{T, N, K, k_pre, h, S, L, topk_ids, topk_w, keep, nullptr, fold_ids, fold_w,
                     loss_cap, flags, om_src, om_w, om_q, wret};
   const bf16_t *xb = static_cast<const bf16_t *>(x), *wb = static_cast<const bf16_t *>(w_router);
-  if (N <= 8) route_small_kernel<8><<<T, 256, 0, s>>>(xb, wb, d, bias, logits_out, a);
+  if (T > kRouteSmallMaxT) {
+    const int blocks = (T + 15) / 16;
+    if (N <= 16) route_block_kernel<1, 8><<<blocks, 512, 0, s>>>(xb, wb, d, bias, logits_out, a);
+    else route_block_kernel<2, 8><<<blocks, 512, 0, s>>>(xb, wb, d, bias, logits_out, a);
+  } else if (N <= 8) route_small_kernel<8><<<T, 256, 0, s>>>(xb, wb, d, bias, logits_out, a);
   else if (N <= 16) route_small_kernel<16><<<T, 256, 0, s>>>(xb, wb, d, bias, logits_out, a);
   else route_small_kernel<32><<<T, 256, 0, s>>>(xb, wb, d, bias, logits_out, a);
   return hipGetLastError();

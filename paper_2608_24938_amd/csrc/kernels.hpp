@@ -24,8 +24,8 @@ hipError_t launch_route_tokens(const float *part, int P, const float *bias, floa
                                int32_t *om_src = nullptr, float *om_w = nullptr,
                                int32_t *om_q = nullptr, float *wret = nullptr);
 // Router logits and the per-token steps of launch_route_tokens in one kernel, for
-// bf16 layers of at most 32 experts and batches of at most 1024 tokens
-// (route_small_fits); x [T, d], w_router [N, d].
+// bf16 layers of at most 32 experts (route_small_fits): one workgroup per token
+// up to 1024 tokens, one per 16 tokens beyond; x [T, d], w_router [N, d].
 bool route_small_fits(int dtype, int N, int T);
 hipError_t launch_route_small(const void *x, const void *w_router, int d, const float *bias,
                               float *logits_out, int T, int N, int K, int k_pre, const float *h,

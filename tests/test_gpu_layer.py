@@ -81,6 +81,8 @@ def _forward_case(shape, T, phase, budget, seed=2):
     # route_small_kernel (router, Top-K and fold in one kernel) for few experts
     (ROUTER24_BF16, 21, "decode", 6), (ROUTER24_BF16, 1, "decode", 2), (ROUTER8_BF16, 64, "decode", 4),
     (ROUTER8_BF16, 37, "dense", 0), (ROUTER24_BF16, 90, "decode", 10), (ROUTER24_BF16, 300, "prefill", 2),
+    # beyond 1024 tokens: one workgroup per 16 tokens (logits over all of d, then routing), ragged last block
+    (ROUTER24_BF16, 1100, "prefill", 2), (ROUTER24_BF16, 1040, "decode", 10), (ROUTER8_BF16, 2050, "dense", 0),
 ])
 def test_forward_matches_oracle(shape, T, phase, budget):
     lp, xs, (S, L, h), dbg, y = _forward_case(shape, T, phase, budget)
