@@ -38,6 +38,11 @@ GLM = dict(d=4096, inter=1408, n=128, k=8, shared=1408)
     (QWEN3, 1024, 16, TILE, TILE),           # decode, 128 tokens, pool of 16 (64 rows per expert)
     (QWEN3, 1024, 64, SKINNY, SKINNY),       # decode, 128 tokens, pool of 64 (16 rows per expert)
     (QWEN3, 4096, 32, WIDE, WIDE),           # decode, 512 tokens, pool of 32 (wide down without a full round)
+    (QWEN3, 2048, 16, TILE, TILE),           # 128 rows per expert but 48 wide tiles, under a quarter round
+    (QWEN3, 2048, 32, TILE, TILE),           # 64 rows per expert: 128x128 down tiles above 48 rows
+    (QWEN3, 1024, 32, TILE, SKINNY),         # 32 rows per expert: skinny down tiles up to 48 rows
+    (QWEN3, 512, 16, TILE, SKINNY),          # 32 rows per expert: 128x128 gate/up tiles above 24 rows
+    (QWEN3, 384, 16, SKINNY, SKINNY),        # 24 rows per expert: skinny gate/up tiles
     (GLM, 64 * 8 + 64, 33, SKINNY, SKINNY),  # decode with the shared expert
     (GLM, 4096 * 4 + 4096, 129, TILE, TILE),  # I = 1408 splits into no 256-wide pairs
 ])
