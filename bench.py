@@ -18,7 +18,10 @@ prefill (8192 tokens, K'=4) and decode (128 tokens, D=16), folded and
 unfolded, timed in the same run.  The
 timed steps record HIP events only at the layer boundaries and around the
 dominant kernel; the per-stage breakdown in the line comes from a second,
-fully instrumented run of the same steps after the timed region.
+fully instrumented run of the same steps after the timed region.  `clock`
+holds the GFX clock the driver reports for each XCD (amd-smi) while prefill
+forwards run back to back after the timed region, and the peak fractions
+against the dense peak at that clock (null without amd-smi).
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload mixtral|qwen3|glm|qwen3-decode]
 
@@ -246,6 +249,12 @@ def main():
     n_groups = shape.n_experts + (1 if shape.shared_inter else 0)
     gu_bytes = (2 * shape.inter * shape.d * n_groups + gu_rows * shape.d + gu_rows * shape.inter) * esz
     traffic = recorded_traffic(args.workload)
+    clock = measured_gfx_clock(
+        lambda: X.moe_forward(layer, x_p, "prefill", kp, S, L, h, y=y_p, workspace=ws_p))
+    if clock is not None:
+        scale = NOMINAL_SCLK_MHZ / clock["mean_mhz"]
+        clock["prefill_frac_at_measured_clock"] = round(tflops / PEAK_BF16_TFLOPS * scale, 4)
+        clock["roofline_frac_at_measured_clock"] = round(gu_tflops / PEAK_BF16_TFLOPS * scale, 4)
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -288,9 +297,48 @@ def main():
                      "per_launch_gflop": round(gu_flops / 1e9, 2), "avg_launch_us": round(gate_up_us, 1)},
         "cpu_baseline": cpu,
         "secondary": secondary,
+        "clock": clock,
     }
     ev.close()
     print(json.dumps(rec), flush=True)
+
+
+NOMINAL_SCLK_MHZ = 2400  # the clock of the dense peak figure
+
+
+def measured_gfx_clock(fwd, seconds=1.5):
+    """The GFX clock of each XCD as the driver reports it (`amd-smi metric -c`), sampled once while
+    fwd() runs back to back (after 0.5 s under the load); None where amd-smi is missing or fails."""
+    import shutil
+    import subprocess
+    import threading
+    import numpy as np
+    import torch
+    exe = shutil.which("amd-smi")
+    if exe is None:
+        return None
+    out = {}
+
+    def sample():
+        time.sleep(0.5)
+        try:
+            out["text"] = subprocess.run([exe, "metric", "-c"], capture_output=True, text=True, timeout=10).stdout
+        except (OSError, subprocess.SubprocessError):
+            pass
+
+    th = threading.Thread(target=sample)
+    t0 = time.time()
+    th.start()
+    while (th.is_alive() or time.time() - t0 < seconds) and time.time() - t0 < 20:
+        for _ in range(10):
+            fwd()
+        torch.cuda.synchronize()
+    th.join(timeout=15)
+    mhz = [int(v) for v in re.findall(r"GFX_\d+:\s+CLK:\s+(\d+)\s*MHz", out.get("text", ""))]
+    if not mhz:
+        return None
+    return {"source": "amd-smi metric -c, sampled during back-to-back prefill forwards", "gfx_mhz": mhz,
+            "mean_mhz": round(float(np.mean(mhz)), 1), "nominal_mhz": NOMINAL_SCLK_MHZ}
 
 
 def secondary_configs(X, ev, steps, warmup):
