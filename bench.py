@@ -19,9 +19,11 @@ unfolded, timed in the same run.  The
 timed steps record HIP events only at the layer boundaries and around the
 dominant kernel; the per-stage breakdown in the line comes from a second,
 fully instrumented run of the same steps after the timed region.  `clock`
-holds the GFX clock the driver reports for each XCD (amd-smi) while prefill
-forwards run back to back after the timed region, and the peak fractions
-against the dense peak at that clock (null without amd-smi).
+holds the GFX clock the driver reports for each XCD (amd-smi, three readings)
+while prefill forwards run back to back after the timed region, and the peak
+fractions against the dense peak at that clock (null without amd-smi, and null
+with `plausible` false when the reading is below the clock that the measured
+gate/up rate needs).
 
     python bench.py [--gpus 1] [--steps 20] [--warmup 5] [--workload mixtral|qwen3|glm|qwen3-decode]
 
@@ -252,9 +254,13 @@ def main():
     clock = measured_gfx_clock(
         lambda: X.moe_forward(layer, x_p, "prefill", kp, S, L, h, y=y_p, workspace=ws_p))
     if clock is not None:
+        # a reading is used only if the measured gate/up rate fits under the dense MFMA rate at
+        # that clock (a lower reading cannot have held while the kernel ran)
         scale = NOMINAL_SCLK_MHZ / clock["mean_mhz"]
-        clock["prefill_frac_at_measured_clock"] = round(tflops / PEAK_BF16_TFLOPS * scale, 4)
-        clock["roofline_frac_at_measured_clock"] = round(gu_tflops / PEAK_BF16_TFLOPS * scale, 4)
+        pf, rf = tflops / PEAK_BF16_TFLOPS * scale, gu_tflops / PEAK_BF16_TFLOPS * scale
+        clock["plausible"] = rf <= 1.0
+        clock["prefill_frac_at_measured_clock"] = round(pf, 4) if rf <= 1.0 else None
+        clock["roofline_frac_at_measured_clock"] = round(rf, 4) if rf <= 1.0 else None
 
     cpu = None
     if not args.no_cpu_baseline:
@@ -306,9 +312,11 @@ def main():
 NOMINAL_SCLK_MHZ = 2400  # the clock of the dense peak figure
 
 
-def measured_gfx_clock(fwd, seconds=1.5):
-    """The GFX clock of each XCD as the driver reports it (`amd-smi metric -c`), sampled once while
-    fwd() runs back to back (after 0.5 s under the load); None where amd-smi is missing or fails."""
+def measured_gfx_clock(fwd, seconds=2.0, samples=3):
+    """The GFX clock of each XCD as the driver reports it (`amd-smi metric -c`), sampled `samples`
+    times while fwd() runs back to back (the first 0.5 s into the load, then one about every 0.3 s
+    after the previous reading returns); None where amd-smi is missing or fails.  mean_mhz is the
+    median over the samples of their mean over the XCDs."""
     import shutil
     import subprocess
     import threading
@@ -317,28 +325,33 @@ def measured_gfx_clock(fwd, seconds=1.5):
     exe = shutil.which("amd-smi")
     if exe is None:
         return None
-    out = {}
+    texts = []
 
     def sample():
         time.sleep(0.5)
-        try:
-            out["text"] = subprocess.run([exe, "metric", "-c"], capture_output=True, text=True, timeout=10).stdout
-        except (OSError, subprocess.SubprocessError):
-            pass
+        for _ in range(samples):
+            try:
+                texts.append(subprocess.run([exe, "metric", "-c"], capture_output=True, text=True, timeout=10).stdout)
+            except (OSError, subprocess.SubprocessError):
+                pass
+            time.sleep(0.3)
 
     th = threading.Thread(target=sample)
     t0 = time.time()
     th.start()
-    while (th.is_alive() or time.time() - t0 < seconds) and time.time() - t0 < 20:
+    while (th.is_alive() or time.time() - t0 < seconds) and time.time() - t0 < 40:
         for _ in range(10):
             fwd()
         torch.cuda.synchronize()
     th.join(timeout=15)
-    mhz = [int(v) for v in re.findall(r"GFX_\d+:\s+CLK:\s+(\d+)\s*MHz", out.get("text", ""))]
-    if not mhz:
+    per = [[int(v) for v in re.findall(r"GFX_\d+:\s+CLK:\s+(\d+)\s*MHz", t)] for t in texts]
+    per = [m for m in per if m]
+    if not per:
         return None
-    return {"source": "amd-smi metric -c, sampled during back-to-back prefill forwards", "gfx_mhz": mhz,
-            "mean_mhz": round(float(np.mean(mhz)), 1), "nominal_mhz": NOMINAL_SCLK_MHZ}
+    means = [float(np.mean(m)) for m in per]
+    return {"source": "amd-smi metric -c, sampled during back-to-back prefill forwards", "gfx_mhz": per,
+            "sample_mean_mhz": [round(v, 1) for v in means], "mean_mhz": round(float(np.median(means)), 1),
+            "nominal_mhz": NOMINAL_SCLK_MHZ}
 
 
 def secondary_configs(X, ev, steps, warmup):

@@ -674,26 +674,31 @@ __global__ __launch_bounds__(64 * KS) void route_block_kernel(const bf16_t *__re
   bf16x8 zero;
 #pragma unroll
   for (int q = 0; q < 8; ++q) zero[q] = (__bf16)0.0f;
-  // the wave's steps in chunks of C, every load of a chunk issued before its
-  // MFMAs (one round trip per chunk); steps past the range re-read its last
-  // step and are not accumulated
-  constexpr int C = 8 / NT;
-  for (int c0 = s0; c0 < s1; c0 += C) {
-    bf16x8 av[C], bv[C][NT];
+  int st = s0;
+  for (; st + 2 <= s1; st += 2) {
+    const int k = st * 32;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(xa + k);
+    const bf16x8 a1 = *reinterpret_cast<const bf16x8 *>(xa + k + 32);
+    bf16x8 b0[NT], b1[NT];
 #pragma unroll
-    for (int q = 0; q < C; ++q) {
-      const int k = min(c0 + q, s1 - 1) * 32;
-      av[q] = *reinterpret_cast<const bf16x8 *>(xa + k);
-#pragma unroll
-      for (int j = 0; j < NT; ++j) bv[q][j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
+    for (int j = 0; j < NT; ++j) {
+      b0[j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
+      b1[j] = *reinterpret_cast<const bf16x8 *>(wrow[j] + k + 32);
     }
 #pragma unroll
-    for (int q = 0; q < C; ++q)
-      if (c0 + q < s1) {
+    for (int j = 0; j < NT; ++j) {
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, live[j] ? b0[j] : zero, acc[j], 0, 0, 0);
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a1, live[j] ? b1[j] : zero, acc[j], 0, 0, 0);
+    }
+  }
+  if (st < s1) {
+    const int k = st * 32;
+    const bf16x8 a0 = *reinterpret_cast<const bf16x8 *>(xa + k);
 #pragma unroll
-        for (int j = 0; j < NT; ++j)
-          acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(av[q], live[j] ? bv[q][j] : zero, acc[j], 0, 0, 0);
-      }
+    for (int j = 0; j < NT; ++j) {
+      const bf16x8 b0 = *reinterpret_cast<const bf16x8 *>(wrow[j] + k);
+      acc[j] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a0, live[j] ? b0 : zero, acc[j], 0, 0, 0);
+    }
   }
   // accumulator i of lane l: token (l / 16) * 4 + i, expert 16 j + l % 16
 #pragma unroll
