@@ -115,6 +115,9 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-secondary", action="store_true",
                     help="skip the Qwen3-shaped prefill and decode timed after the main workload")
+    ap.add_argument("--no-clock", action="store_true",
+                    help="skip the amd-smi clock readings (for runs under a profiler, whose preloaded "
+                         "library must not reach the amd-smi child process)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run one plain 1 GiB device copy (the scale for the FETCH_SIZE/WRITE_SIZE counters)")
     ap.add_argument("--prof-summary", metavar="DIR",
@@ -251,7 +254,7 @@ def main():
     n_groups = shape.n_experts + (1 if shape.shared_inter else 0)
     gu_bytes = (2 * shape.inter * shape.d * n_groups + gu_rows * shape.d + gu_rows * shape.inter) * esz
     traffic = recorded_traffic(args.workload)
-    clock = measured_gfx_clock(
+    clock = None if args.no_clock else measured_gfx_clock(
         lambda: X.moe_forward(layer, x_p, "prefill", kp, S, L, h, y=y_p, workspace=ws_p))
     if clock is not None:
         # a reading is used only if the measured gate/up rate fits under the dense MFMA rate at
